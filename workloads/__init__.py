@@ -1,0 +1,137 @@
+"""Seeded synthetic attention workloads, shared by the oracle tests, the GPU tests and the benchmark.
+
+This module holds shapes, seeds, random draws and measurement formulas only. It contains none of
+the attention arithmetic (no products, no softmax): the fp64 oracle and the HIP kernels each
+implement that on their own, and both take their inputs from here.
+
+Inputs follow the paper's evaluation practice: every element of Q, K and V is drawn i.i.d. from
+N(0, sigma^2) with sigma = 1 (Sec. "Numerical Stability", the regime of normalised activations),
+at shapes of public LLM attention configurations (Sec. "Generality Across LLM Configurations",
+Table 6). Draws are fp32 from torch's CPU generator (mt19937), seeded per workload, in the order
+Q, K, V, then rounded to bfloat16 with round-to-nearest-even (torch's ``.to``).
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, replace
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One attention problem in contiguous BHSD layout.
+
+    Q: [B][Hq][Sq][dqk], K: [B][Hkv][Sk][dqk], V: [B][Hkv][Sk][dv], O: [B][Hq][Sq][dv],
+    LSE: fp32 [B][Hq][Sq]. Query head h reads key/value head h // (Hq // Hkv).
+    """
+
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    Sq: int
+    Sk: int
+    dqk: int
+    dv: int
+    causal: bool
+    scale: float
+    seed: int
+    sigma: float = 1.0
+
+    @property
+    def group(self) -> int:
+        return self.Hq // self.Hkv if self.Hkv else 0
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+def _wl(idx: int, name: str, B, Hq, Hkv, S, dqk, dv, causal) -> Workload:
+    return Workload(name=name, B=B, Hq=Hq, Hkv=Hkv, Sq=S, Sk=S, dqk=dqk, dv=dv, causal=causal,
+                    scale=1.0 / math.sqrt(dqk), seed=1000 + idx)
+
+
+#: The five benchmark workloads, numbered 1..5.
+CONFIGS: Dict[int, Workload] = {
+    1: _wl(1, "single-head B1 H1 S256 d64 non-causal", 1, 1, 1, 256, 64, 64, False),
+    2: _wl(2, "BERT-base-shaped B8 H12 S512 d64 non-causal", 8, 12, 12, 512, 64, 64, False),
+    3: _wl(3, "Llama-style GQA prefill B1 Hq32 Hkv8 S8192 d128 causal", 1, 32, 8, 8192, 128, 128, True),
+    4: _wl(4, "DeepSeek-style wide-head prefill B1 H128 S4096 dqk192 dv128 causal",
+           1, 128, 128, 4096, 192, 128, True),
+    5: _wl(5, "long-context GQA prefill B1 Hq32 Hkv8 S131072 d128 causal", 1, 32, 8, 131072, 128, 128, True),
+}
+
+
+def make_inputs(w: Workload, device: str = "cpu") -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Draw Q, K, V (bf16, contiguous BHSD) for workload ``w`` from its seed.
+
+    The fp32 draws are rounded to bf16 before anything else sees them; the bf16 tensors are
+    the exact inputs of both the oracle and the GPU path.
+    """
+    g = torch.Generator(device="cpu")
+    g.manual_seed(w.seed)
+    out = []
+    for shape in ((w.B, w.Hq, w.Sq, w.dqk), (w.B, w.Hkv, w.Sk, w.dqk), (w.B, w.Hkv, w.Sk, w.dv)):
+        x = torch.randn(shape, dtype=torch.float32, generator=g)
+        if w.sigma != 1.0:
+            x.mul_(w.sigma)
+        out.append(x.to(torch.bfloat16).contiguous())
+        del x
+    q, k, v = out
+    if device != "cpu":
+        q, k, v = q.to(device), k.to(device), v.to(device)
+    return q, k, v
+
+
+def sample_rows(w: Workload, n: int = 64, seed_base: int = 2000) -> List[np.ndarray]:
+    """Seeded query-row subset per query head (used where the full output is too large for the oracle).
+
+    For each head h in order: ``sorted(rng.choice(Sq, n))`` without replacement, plus rows 0 and Sq-1.
+    The generator is ``numpy.random.default_rng(seed_base + (seed - 1000))``.
+    """
+    rng = np.random.default_rng(seed_base + (w.seed - 1000))
+    rows = []
+    for _ in range(w.B * w.Hq):
+        r = rng.choice(w.Sq, size=min(n, w.Sq), replace=False)
+        r = np.union1d(r, [0, w.Sq - 1]) if w.Sq > 0 else r
+        rows.append(np.asarray(sorted(r), dtype=np.int64))
+    return rows
+
+
+def metric_flops(w: Workload) -> float:
+    """GEMM FLOPs of one forward pass in the metric's convention.
+
+    2*B*Hq*Sq*Sk*(dqk + dv): the two contractions Q.K^T and P.V (Sec. "Operational Intensity
+    Constraint"), halved exactly when causal.
+    """
+    f = 2.0 * w.B * w.Hq * w.Sq * w.Sk * (w.dqk + w.dv)
+    return f * 0.5 if w.causal else f
+
+
+def paper_flops(H: int, Lq: int, Lk: int, dk: int, dv: int, B: int = 1) -> float:
+    """Effective GEMM work of the paper's throughput formula (Sec. 6.1, P_effGEMM numerator).
+
+    2*H*Lq*Lk*(dk+dv), never halved for causal masking.
+    """
+    return 2.0 * B * H * Lq * Lk * (dk + dv)
+
+
+def algorithmic_bytes(w: Workload, with_lse: bool = True) -> int:
+    """HBM bytes a fused forward must move at minimum: read Q, K, V once, write O (bf16) and LSE (fp32)."""
+    q = w.B * w.Hq * w.Sq * w.dqk
+    k = w.B * w.Hkv * w.Sk * w.dqk
+    v = w.B * w.Hkv * w.Sk * w.dv
+    o = w.B * w.Hq * w.Sq * w.dv
+    lse = w.B * w.Hq * w.Sq if with_lse else 0
+    return 2 * (q + k + v + o) + 4 * lse
+
+
+def small(name: str, B=1, Hq=1, Hkv=1, Sq=64, Sk=64, dqk=64, dv=64, causal=False,
+          scale: Optional[float] = None, seed: int = 7, sigma: float = 1.0) -> Workload:
+    """An ad-hoc workload for tests (odd shapes, edge cases)."""
+    return Workload(name=name, B=B, Hq=Hq, Hkv=Hkv, Sq=Sq, Sk=Sk, dqk=dqk, dv=dv, causal=causal,
+                    scale=(1.0 / math.sqrt(dqk)) if scale is None else scale, seed=seed, sigma=sigma)
