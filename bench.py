@@ -1,0 +1,223 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused attention forward on one MI355X.
+
+One step = one forward pass of the whole hot path (one kernel launch) over one batch of seeded
+synthetic input already resident in HBM. Prints ONE JSON line:
+
+* value      -- whole-job GEMM TFLOP/s: 2*B*Hq*Sq*Sk*(d_qk+d_v) (halved for causal) per step, over
+                the wall-clock time of the timed steps (bracketed by device synchronisation)
+* roofline   -- the kernel's achieved TFLOP/s from HIP events around each launch on the launch
+                stream, against the bf16 dense MFMA peak; HBM traffic from the committed rocprofv3
+                counter summary when it was taken on the current kernel source
+* cpu_baseline -- the fp64 oracle timed on this host on a bounded sample of the same workload
+* parity     -- a few seeded rows per head compared with the oracle (outside the timed region)
+
+Default workload: the Llama-style GQA prefill, B1 Hq32 Hkv8 S8192 d128 causal (config 3).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # 256 CUs x 4096 dense bf16 FLOP/clk/CU x 2.4 GHz
+KERNEL_SOURCES = ["paper_2609_21264_amd/csrc/fa_fwd_kernel.hip", "paper_2609_21264_amd/csrc/fa_api.hip",
+                  "paper_2609_21264_amd/csrc/fa_internal.h"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(config: int):
+    """HBM bytes per launch from the committed counter summary, if it matches the current kernel."""
+    path = os.path.join(ROOT, "profiles", f"fa_fwd_config{config}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        m = re.match(r"^\s*([a-z_]+)\s*[:=]\s*([0-9a-fA-Fx.eE+-]+)\s*$", line)
+        if m:
+            fields[m.group(1)] = m.group(2)
+    if fields.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, q, k, v, budget_s: float):
+    """Time the fp64 oracle on whole query heads (all rows) until ``budget_s`` has elapsed."""
+    import numpy as np
+
+    from oracle import bf16_bits_to_f64, naive_attention_rows
+
+    def f64(t):
+        return bf16_bits_to_f64(t.contiguous().view(__import__("torch").int16).numpy())
+
+    threads = os.cpu_count()
+    try:
+        import threadpoolctl
+        (np.ones((4, 4)) @ np.ones((4, 4)))
+        info = threadpoolctl.threadpool_info()
+        if info:
+            threads = max(i["num_threads"] for i in info)
+    except Exception:
+        pass
+    rows_all = np.arange(w.Sq)
+    done_heads, t_oracle = 0, 0.0
+    for idx in range(w.B * w.Hq):
+        b, h = divmod(idx, w.Hq)
+        t0 = time.perf_counter()
+        naive_attention_rows(lambda bb, hh, r: f64(q[bb, hh]), lambda bb, g: f64(k[bb, g]),
+                             lambda bb, g: f64(v[bb, g]), 1, 1, 1, w.Sq, w.scale, w.causal, [rows_all])
+        t_oracle += time.perf_counter() - t0
+        done_heads += 1
+        if t_oracle >= budget_s:
+            break
+    frac = done_heads / (w.B * w.Hq)
+    import workloads as W
+    tflops = W.metric_flops(w) * frac / t_oracle / 1e12
+    return {"value": tflops, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done_heads} of {w.B * w.Hq} query heads, all {w.Sq} rows each "
+                      f"({t_oracle:.1f} s of fp64 NumPy; metric FLOPs of the sample)"}
+
+
+def parity_sample(w, q, k, v, o, lse, rows_per_head: int = 4):
+    import numpy as np
+
+    import workloads as W
+    from oracle import bf16_bits_to_f64, naive_attention_rows
+
+    def f64(t):
+        return bf16_bits_to_f64(t.contiguous().view(__import__("torch").int16).numpy())
+
+    rows = W.sample_rows(w, n=rows_per_head, seed_base=3000)
+    res = naive_attention_rows(lambda b, h, r: f64(q[b, h][r]), lambda b, g: f64(k[b, g]),
+                               lambda b, g: f64(v[b, g]), w.B, w.Hq, w.Hkv, w.Sq, w.scale, w.causal, rows)
+    oc, lc = o.cpu(), lse.cpu()
+    max_abs, lse_max, n = 0.0, 0.0, 0
+    for idx, (o_ref, l_ref) in enumerate(res):
+        b, h = divmod(idx, w.Hq)
+        r = rows[idx]
+        og = f64(oc[b, h][r])
+        max_abs = max(max_abs, float(np.abs(og - o_ref).max()))
+        fin = np.isfinite(l_ref)
+        if fin.any():
+            lse_max = max(lse_max, float(np.abs(lc[b, h][r].double().numpy()[fin] - l_ref[fin]).max()))
+        n += len(r)
+    return {"rows_checked": n, "max_abs": max_abs, "lse_max_abs": lse_max,
+            "pass": bool(max_abs <= 2e-2 and lse_max <= 1e-3)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the fused attention kernel runs on a "
+              "single MI355X and this build has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_21264_amd as fa
+    import workloads as W
+
+    w = W.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print(f"[bench] workload {args.config}: {w.name}", file=sys.stderr, flush=True)
+    q_cpu, k_cpu, v_cpu = W.make_inputs(w)
+    q, k, v = q_cpu.to(dev), k_cpu.to(dev), v_cpu.to(dev)
+    o = torch.empty((w.B, w.Hq, w.Sq, w.dv), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    handle = stream.cuda_stream
+
+    def step():
+        st = fa.fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), w.B, w.Hq,
+                          w.Hkv, w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, handle)
+        if st != 0:
+            raise fa.FaError(st)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s, e in ev:
+        s.record(stream)
+        step()
+        e.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    launch_ms = [s.elapsed_time(e) for s, e in ev]
+    print(f"[bench] timed {args.steps} steps in {wall:.4f} s", file=sys.stderr, flush=True)
+
+    flops = W.metric_flops(w)
+    value = flops * args.steps / wall / 1e12
+    avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+    achieved = flops / avg_launch_s / 1e12
+    traffic = traffic_from_profile(args.config)
+
+    parity = parity_sample(w, q_cpu, k_cpu, v_cpu, o, lse)
+    print(f"[bench] parity sample: {parity}", file=sys.stderr, flush=True)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, q_cpu, k_cpu, v_cpu, args.cpu_budget)
+        print(f"[bench] cpu baseline: {cpu}", file=sys.stderr, flush=True)
+
+    out = {
+        "metric": "attention fwd GEMM TFLOP/s on 1 MI355X; % of bf16 MFMA peak",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Sq": w.Sq, "Sk": w.Sk,
+                   "d_qk": w.dqk, "d_v": w.dv, "causal": w.causal, "scale": w.scale, "seed": w.seed},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic,
+                     "kernel_ms": {"mean": round(sum(launch_ms) / len(launch_ms), 4), "min": round(min(launch_ms), 4)},
+                     "algorithmic_flops_per_launch": flops,
+                     "algorithmic_bytes_per_launch": W.algorithmic_bytes(w)},
+        "cpu_baseline": cpu,
+        "parity": parity,
+        "kernel_source": kernel_source_hash(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

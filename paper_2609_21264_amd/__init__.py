@@ -1,0 +1,101 @@
+"""Fused attention forward for AMD Instinct MI355X (gfx950).
+
+A thin Python binding over ``libfa.so``, whose C ABI is declared in ``include/fa.h``. PyTorch only
+supplies device memory and the stream; every step of the computation runs in the library's HIP
+kernel. The functions below marshal arguments and translate status codes, nothing more.
+
+* :func:`fa_fwd`, :func:`fa_fwd_ex`, :func:`fa_status_str`, :func:`fa_block_rows` -- the C entry
+  points under the same names, taking raw device pointers (ints) and sizes.
+* :func:`forward` -- convenience wrapper over torch tensors.
+"""
+
+from __future__ import annotations
+
+import math
+from typing import Optional
+
+from . import _lib
+from ._lib import (FA_ERR_BAD_SCALE, FA_ERR_BAD_SHAPE, FA_ERR_HIP, FA_ERR_NULL_POINTER,  # noqa: F401
+                   FA_ERR_UNSUPPORTED, FA_OK, LIB_PATH)
+
+__all__ = ["fa_fwd", "fa_fwd_ex", "fa_status_str", "fa_block_rows", "forward", "FaError", "LIB_PATH"]
+
+
+class FaError(RuntimeError):
+    """A non-FA_OK status from the library."""
+
+    def __init__(self, status: int):
+        self.status = status
+        super().__init__(f"{fa_status_str(status)} ({status})")
+
+
+def fa_status_str(status: int) -> str:
+    return _lib.load().fa_status_str(int(status)).decode()
+
+
+def fa_block_rows(d_qk: int, d_v: int, causal: bool) -> int:
+    return int(_lib.load().fa_block_rows(int(d_qk), int(d_v), int(bool(causal))))
+
+
+def fa_fwd(Q: int, K: int, V: int, O: int, B: int, Hq: int, Hkv: int, Sq: int, Sk: int, d: int,
+           scale: float, causal: bool, stream: int) -> int:
+    """C ``fa_fwd``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_fwd(Q, K, V, O, B, Hq, Hkv, Sq, Sk, d, float(scale), int(bool(causal)), stream))
+
+
+def fa_fwd_ex(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, Hq: int, Hkv: int, Sq: int,
+              Sk: int, d_qk: int, d_v: int, scale: float, causal: bool, stream: int) -> int:
+    """C ``fa_fwd_ex``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_fwd_ex(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, float(scale),
+                                     int(bool(causal)), stream))
+
+
+def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return_lse: bool = False,
+            out=None, lse=None, stream=None):
+    """Attention forward over contiguous bf16 BHSD torch tensors on one GPU.
+
+    q [B, Hq, Sq, d_qk], k [B, Hkv, Sk, d_qk], v [B, Hkv, Sk, d_v]; returns O [B, Hq, Sq, d_v] (bf16)
+    and, with ``return_lse``, LSE [B, Hq, Sq] (float32, natural log). ``scale`` defaults to
+    1/sqrt(d_qk). The kernel is enqueued on ``stream`` (default: torch's current stream); the call
+    does not synchronise.
+    """
+    import torch
+
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not isinstance(t, torch.Tensor) or t.dim() != 4:
+            raise ValueError(f"{name} must be a 4-d torch tensor (BHSD)")
+        if t.dtype != torch.bfloat16:
+            raise ValueError(f"{name} must be bfloat16")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on a GPU")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if not (q.device == k.device == v.device):
+        raise ValueError("q, k, v must be on the same device")
+    B, Hq, Sq, dqk = q.shape
+    Bk, Hkv, Sk, dk = k.shape
+    if Bk != B or dk != dqk or v.shape[:3] != k.shape[:3]:
+        raise ValueError(f"inconsistent shapes q{tuple(q.shape)} k{tuple(k.shape)} v{tuple(v.shape)}")
+    dv = v.shape[3]
+    if scale is None:
+        scale = 1.0 / math.sqrt(dqk)
+    if out is None:
+        out = torch.empty((B, Hq, Sq, dv), dtype=torch.bfloat16, device=q.device)
+    elif out.shape != (B, Hq, Sq, dv) or out.dtype != torch.bfloat16 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous bf16 tensor of shape [B, Hq, Sq, d_v]")
+    if return_lse and lse is None:
+        lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.shape != (B, Hq, Sq) or lse.dtype != torch.float32 or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 tensor of shape [B, Hq, Sq]")
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    with torch.cuda.device(q.device):
+        st = fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                       lse.data_ptr() if lse is not None else None,
+                       B, Hq, Hkv, Sq, Sk, dqk, dv, scale, causal, handle)
+    if st != FA_OK:
+        if st in (FA_ERR_NULL_POINTER, FA_ERR_BAD_SHAPE, FA_ERR_UNSUPPORTED, FA_ERR_BAD_SCALE):
+            raise ValueError(f"fa_fwd_ex rejected the arguments: {fa_status_str(st)}")
+        raise FaError(st)
+    return (out, lse) if return_lse else out

@@ -1,0 +1,50 @@
+"""ctypes loader for libfa.so (the C ABI declared in include/fa.h).
+
+The library must already be built (``python -m paper_2609_21264_amd.build``). There is no fallback:
+if it is missing or fails to load, an ImportError names the problem.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libfa.so")
+
+# Status codes of fa_status_t.
+FA_OK = 0
+FA_ERR_NULL_POINTER = 1
+FA_ERR_BAD_SHAPE = 2
+FA_ERR_UNSUPPORTED = 3
+FA_ERR_BAD_SCALE = 4
+FA_ERR_HIP = 5
+
+#: Symbols include/fa.h declares.
+EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_status_str", "fa_block_rows")
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libfa.so once. torch is imported first so that the HIP runtime torch already mapped is the
+    one libfa.so binds to (both carry the soname libamdhip64.so.7); stream handles then mix."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (maps torch's HIP runtime before libfa.so resolves its own)
+
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_21264_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+    lib.fa_fwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp]
+    lib.fa_fwd.restype = i
+    lib.fa_fwd_ex.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, vp]
+    lib.fa_fwd_ex.restype = i
+    lib.fa_status_str.argtypes = [i]
+    lib.fa_status_str.restype = ctypes.c_char_p
+    lib.fa_block_rows.argtypes = [i, i, i]
+    lib.fa_block_rows.restype = i
+    _lib = lib
+    return lib

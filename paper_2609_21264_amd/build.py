@@ -1,0 +1,76 @@
+"""Build step for the HIP library ``libfa.so`` (gfx950).
+
+Run ``python -m paper_2609_21264_amd.build`` (or call :func:`build`). hipcc cross-compiles for gfx950
+on any machine with ROCm; no GPU is needed. The library is written next to this file, in-tree.
+"""
+
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG_DIR)
+CSRC = os.path.join(PKG_DIR, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB_NAME = "libfa.so"
+LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
+SOURCES = ["fa_api.hip", "fa_fwd_kernel.hip"]
+ARCH = "gfx950"
+
+
+def hipcc() -> str:
+    cand = [os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"]
+    for c in cand:
+        if c and os.path.exists(c):
+            return c
+    raise RuntimeError("hipcc not found: ROCm is required to build libfa.so")
+
+
+def compile_command(out: str, extra=()) -> list:
+    return [
+        hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+        # Packed fp32 VALU instructions are kept out of the generated code.
+        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # Score MFMAs in VGPR form (the softmax reads them); the P V accumulators are pinned to
+        # AGPRs by inline asm in the kernel.
+        "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+        "-Wall", "-Wno-unused-command-line-argument",
+        "-I", INCLUDE, "-I", CSRC,
+        "-Wl,-rpath,/opt/rocm/lib",
+        *extra,
+        "-o", out,
+        *[os.path.join(CSRC, s) for s in SOURCES],
+    ]
+
+
+def build(verbose: bool = False, resource_usage: bool = False) -> str:
+    """Compile libfa.so for gfx950 into the package directory; returns its path."""
+    extra = ["-Rpass-analysis=kernel-resource-usage"] if resource_usage else []
+    fd, tmp = tempfile.mkstemp(prefix=".libfa.", suffix=".so.tmp", dir=PKG_DIR)
+    os.close(fd)
+    try:
+        cmd = compile_command(tmp, extra)
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        out = (res.stdout or "") + (res.stderr or "")
+        # hipcc's host pass does not know the packed-fp32 feature name; that warning is expected.
+        lines = [ln for ln in out.splitlines() if "packed-fp32-ops" not in ln or "error" in ln]
+        if res.returncode != 0:
+            raise RuntimeError("hipcc failed:\n" + "\n".join(lines))
+        if verbose or resource_usage:
+            print("\n".join(lines), flush=True)
+        os.replace(tmp, LIB_PATH)
+    finally:
+        if os.path.exists(tmp):
+            os.unlink(tmp)
+    return LIB_PATH
+
+
+if __name__ == "__main__":
+    build(verbose="-v" in sys.argv, resource_usage="--resource-usage" in sys.argv)
+    print(LIB_PATH)

@@ -1,0 +1,32 @@
+// Internal interface between the C-ABI layer (fa_api.hip) and the kernel launchers
+// (fa_fwd_kernel.hip). Not installed; callers use include/fa.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fa {
+
+// Arguments of one forward launch, after host-side validation.
+struct FwdParams {
+  const uint16_t* q;  // bf16 [B][Hq][Sq][d_qk]
+  const uint16_t* k;  // bf16 [B][Hkv][Sk][d_qk]
+  const uint16_t* v;  // bf16 [B][Hkv][Sk][d_v]
+  uint16_t* o;        // bf16 [B][Hq][Sq][d_v]
+  float* lse;         // fp32 [B][Hq][Sq] or nullptr
+  int batch, hq, hkv, sq, sk;
+  int group;          // Hq / Hkv
+  float c;            // |scale| * log2(e), at least FLT_MIN so that a masked -inf score stays -inf
+  uint32_t qsign;     // 0x80008000 when scale < 0: K is negated (exactly) and c = |scale| log2 e
+  int n_qtiles;       // ceil(Sq / block rows)
+  int n_wg;           // batch * hq * n_qtiles
+};
+
+// Query rows per workgroup of the kernel instance for (d_qk, d_v, causal); 0 if not compiled in.
+int block_rows(int d_qk, int d_v, bool causal);
+
+// Enqueue the forward kernel for (d_qk, d_v, causal) on `stream`. Requires Sq > 0, B*Hq > 0 and a
+// grid that fits; fills n_qtiles / n_wg itself. Returns the launch status of the HIP runtime.
+hipError_t launch_forward(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream);
+
+}  // namespace fa

@@ -1,0 +1,85 @@
+"""Helpers shared by the GPU parity tests: run the HIP path, run the oracle, compare.
+
+Acceptance bar (fixed for this project): the bf16 output, widened exactly to float64, is within
+max-abs 2e-2 and mean-abs 2e-3 of the fp64 oracle over all compared elements, and every row's
+log-sum-exp is within 1e-3 (rows with no visible key must be -inf on both sides, with O = 0).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import paper_2609_21264_amd as fa
+import workloads as W
+from oracle import bf16_bits_to_f64, naive_attention, naive_attention_rows
+
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+LSE_ABS = 1e-3
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    """Exact float64 view of a bf16 tensor, through the oracle's own bit decoder."""
+    return bf16_bits_to_f64(t.detach().cpu().contiguous().view(torch.int16).numpy())
+
+
+def run_gpu(q, k, v, w: W.Workload, device="cuda:0", stream=None):
+    qd, kd, vd = q.to(device), k.to(device), v.to(device)
+    o, lse = fa.forward(qd, kd, vd, causal=w.causal, scale=w.scale, return_lse=True, stream=stream)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def compare(o_gpu: np.ndarray, lse_gpu: np.ndarray, o_ref: np.ndarray, lse_ref: np.ndarray, what="",
+            v_scale: float = 1.0):
+    """Assert the acceptance bar; returns (max_abs, mean_abs, lse_max).
+
+    The output bars are stated for unit-variance inputs. O is linear in V, so for inputs whose values
+    are drawn with standard deviation sigma the O bars scale by ``v_scale = max(1, sigma)``; the LSE
+    bar does not depend on V.
+    """
+    assert o_gpu.shape == o_ref.shape, (o_gpu.shape, o_ref.shape)
+    assert np.all(np.isfinite(o_gpu)), f"{what}: non-finite output"
+    err = np.abs(o_gpu - o_ref)
+    max_abs = float(err.max()) if err.size else 0.0
+    mean_abs = float(err.mean()) if err.size else 0.0
+    empty_ref = np.isneginf(lse_ref)
+    assert np.array_equal(np.isneginf(lse_gpu), empty_ref), f"{what}: -inf LSE rows differ"
+    fin = ~empty_ref
+    lse_max = float(np.abs(lse_gpu[fin] - lse_ref[fin]).max()) if fin.any() else 0.0
+    assert max_abs <= MAX_ABS * v_scale, f"{what}: max-abs {max_abs:.3e}"
+    assert mean_abs <= MEAN_ABS * v_scale, f"{what}: mean-abs {mean_abs:.3e}"
+    assert lse_max <= LSE_ABS, f"{what}: LSE max-abs {lse_max:.3e}"
+    if empty_ref.any():
+        assert np.all(o_gpu[empty_ref] == 0.0), f"{what}: rows with no visible key must be 0"
+    return max_abs, mean_abs, lse_max
+
+
+def check_full(w: W.Workload, device="cuda:0"):
+    """Every output element of workload ``w`` against the naive oracle."""
+    q, k, v = W.make_inputs(w)
+    o, lse = run_gpu(q, k, v, w, device)
+    o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), to_f64(v), w.scale, w.causal)
+    return compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name, max(1.0, w.sigma))
+
+
+def check_rows(w: W.Workload, rows_per_head: int, device="cuda:0", inputs=None):
+    """A seeded subset of query rows of every (batch, head), plus rows 0 and Sq-1, against the oracle."""
+    q, k, v = inputs if inputs is not None else W.make_inputs(w)
+    o, lse = run_gpu(q, k, v, w, device)
+    o_cpu, lse_cpu = o.cpu(), lse.cpu()
+    rows = W.sample_rows(w, n=rows_per_head)
+    res = naive_attention_rows(lambda b, h, r: to_f64(q[b, h, torch.as_tensor(r)]),
+                               lambda b, g: to_f64(k[b, g]), lambda b, g: to_f64(v[b, g]),
+                               w.B, w.Hq, w.Hkv, w.Sq, w.scale, w.causal, rows)
+    og, lg, orf, lrf = [], [], [], []
+    for idx, (o_ref, lse_ref) in enumerate(res):
+        b, h = divmod(idx, w.Hq)
+        r = torch.as_tensor(rows[idx])
+        og.append(to_f64(o_cpu[b, h, r]))
+        lg.append(lse_cpu[b, h, r].double().numpy())
+        orf.append(o_ref)
+        lrf.append(lse_ref)
+    return compare(np.concatenate(og), np.concatenate(lg), np.concatenate(orf), np.concatenate(lrf), w.name,
+                   max(1.0, w.sigma))
