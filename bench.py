@@ -131,6 +131,9 @@ def main():
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after the timed steps, run 3 plain device-to-device copies of MIB MiB (a reference "
+                         "kernel of known traffic for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -182,6 +185,17 @@ def main():
     avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
     achieved = flops / avg_launch_s / 1e12
     traffic = traffic_from_profile(args.config)
+
+    if args.copy_calibration > 0:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: 3 x {args.copy_calibration} MiB device copies", file=sys.stderr, flush=True)
+        del src, dst
 
     parity = parity_sample(w, q_cpu, k_cpu, v_cpu, o, lse)
     print(f"[bench] parity sample: {parity}", file=sys.stderr, flush=True)

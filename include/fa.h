@@ -7,8 +7,8 @@
  *
  * computed in one kernel launch: the score tile S = Q K^T never leaves the chip; an online softmax
  * keeps a running row max and row sum and rescales the partial P V accumulation (Alg. 1, Sec. 2.1).
- * The query heads h of one group share key/value head g (grouped-query attention, Sec. 4 and
- * Sec. 6.3). With causal masking, key j is visible to query i iff j <= i + (Sk - Sq) (bottom-right
+ * The query heads h of one group share key/value head g (grouped-query attention, Sec. 4.4 and
+ * Sec. 6.5). With causal masking, key j is visible to query i iff j <= i + (Sk - Sq) (bottom-right
  * alignment; the usual j <= i when Sq == Sk).
  *
  * Element types: Q, K, V and O are IEEE bfloat16 bit patterns (torch.bfloat16). LSE is float32.
