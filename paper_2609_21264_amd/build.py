@@ -38,6 +38,9 @@ def compile_command(out: str, extra=()) -> list:
         # Score MFMAs in VGPR form (the softmax reads them); the P V accumulators are pinned to
         # AGPRs by inline asm in the kernel.
         "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+        # The pipelined step is one fully unrolled sequence of MFMA slots; the default limit for
+        # "#pragma unroll" stops short of it for the widest head dimension.
+        "-mllvm", "-pragma-unroll-threshold=50000",
         "-Wall", "-Wno-unused-command-line-argument",
         "-I", INCLUDE, "-I", CSRC,
         "-Wl,-rpath,/opt/rocm/lib",
