@@ -49,8 +49,8 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
   p.sq = Sq;
   p.sk = Sk;
   p.group = Hq / Hkv;
-  p.c = c < FLT_MIN ? FLT_MIN : static_cast<float>(c);
-  p.qsign = scale < 0.f ? 0x80008000u : 0u;
+  const float cmag = c < FLT_MIN ? FLT_MIN : static_cast<float>(c);
+  p.cs = scale < 0.f ? -cmag : cmag;
   const hipError_t err = fa::launch_forward(p, d_qk, d_v, causal != 0, static_cast<hipStream_t>(stream));
   return err == hipSuccess ? FA_OK : FA_ERR_HIP;
 }

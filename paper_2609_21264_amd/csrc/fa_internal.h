@@ -16,8 +16,8 @@ struct FwdParams {
   float* lse;         // fp32 [B][Hq][Sq] or nullptr
   int batch, hq, hkv, sq, sk;
   int group;          // Hq / Hkv
-  float c;            // |scale| * log2(e), at least FLT_MIN so that a masked -inf score stays -inf
-  uint32_t qsign;     // 0x80008000 when scale < 0: K is negated (exactly) and c = |scale| log2 e
+  float cs;           // scale * log2(e), magnitude at least FLT_MIN so that an infinite (masked)
+                      // score stays infinite; negative when scale < 0
   int n_qtiles;       // ceil(Sq / block rows)
   int n_wg;           // batch * hq * n_qtiles
 };
