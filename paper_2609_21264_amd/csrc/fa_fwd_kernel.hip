@@ -53,6 +53,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
+#ifndef FA_KPF
+#define FA_KPF 2
+#endif
+#ifndef FA_VPF
+#define FA_VPF 4
+#endif
+
 constexpr float kLn2 = 0.69314718055994530942f;
 // A tile's exponentials are accepted when every lane's sum of them is at most 2^8: then no
 // probability exceeds 2^8 relative to the reference maximum.
@@ -106,12 +113,12 @@ __device__ __forceinline__ void agpr_fence(f32x16& acc) {
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+a"(acc));
 }
 // 16 bytes of Q straight into an AGPR tuple (only read as an MFMA operand, so it never needs a VGPR
-// copy). Waits for all of this wave's loads before returning.
-__device__ __forceinline__ bf16x8 load_q(const void* ptr) {
-  bf16x8 r;
-  asm volatile("global_load_dwordx4 %0, %1, off\n\ts_waitcnt vmcnt(0)" : "=a"(r) : "v"(ptr) : "memory");
-  return r;
+// copy). The load is not waited for here: the caller waits on vmcnt and then passes the value
+// through q_ready(), which keeps every read of it after that wait.
+__device__ __forceinline__ void load_q(bf16x8& r, const void* ptr) {
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=a"(r) : "v"(ptr) : "memory");
 }
+__device__ __forceinline__ void q_ready(bf16x8& r) { asm volatile("" : "+a"(r)); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   f32x2 f = {lo, hi};
@@ -191,13 +198,23 @@ struct TileLoader {
       voff[i] = (uint32_t)(row * CH + ((pch % CH) ^ swz(row))) * 16u;
     }
   }
-  // Issue the loads of the tile whose first row is key n0 (0 <= n0 < Sk) into `slot`.
-  __device__ __forceinline__ void issue(int n0, unsigned char* slot, int wave) const {
+  // Buffer of the tile whose first row is key n0 (0 <= n0 < Sk), and this wave's LDS base in `slot`.
+  __device__ __forceinline__ u32x4 rsrc(int n0) const {
     const uint64_t base = head + (uint64_t)n0 * kRowBytes;
-    const u32x4 rsrc = {(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, (rows - (uint32_t)n0) * kRowBytes,
-                        0x00020000u};
+    return u32x4{(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, (rows - (uint32_t)n0) * kRowBytes, 0x00020000u};
+  }
+  __device__ __forceinline__ uint32_t lds(unsigned char* slot, int wave) const {
+    return lds_offset(slot + wave * NI * 1024);
+  }
+  __device__ __forceinline__ void issue_one(const u32x4& r, uint32_t l, int i) const {
+    dma16_buffer(r, voff[i], l + i * 1024);
+  }
+  // Issue all loads of the tile at key n0 into `slot`.
+  __device__ __forceinline__ void issue(int n0, unsigned char* slot, int wave) const {
+    const u32x4 r = rsrc(n0);
+    const uint32_t l = lds(slot, wave);
 #pragma unroll
-    for (int i = 0; i < NI; ++i) dma16_buffer(rsrc, voff[i], lds_offset(slot + (wave * NI + i) * 1024));
+    for (int i = 0; i < NI; ++i) issue_one(r, l, i);
   }
 };
 
@@ -250,8 +267,8 @@ struct Attn {
   static constexpr int NSL = NMS + NMP;     // MFMA slots per step
   static constexpr int NEP = KB * QB * 8;   // exponential pairs per lane per tile
   static constexpr int NVF = PS * DB;       // V fragments per tile
-  static constexpr int KPF = 2;             // K fragments read ahead
-  static constexpr int VPF = 2;             // V fragments read ahead
+  static constexpr int KPF = FA_KPF;        // K fragments read ahead
+  static constexpr int VPF = FA_VPF;        // V fragments read ahead
 
   int i32, h, qw, diag, sk;
   const uint16_t* kg;  // this workgroup's K head in global memory (rebase only)
@@ -270,6 +287,11 @@ struct Attn {
   // overlap in registers only partly.
   static constexpr int E0 = NMP / PS;
   static_assert(NSL >= 5 * E0, "exponentials of chunk c must follow the P V MFMAs of chunk c");
+  static constexpr bool at_most_two_pairs_per_slot() {
+    for (int sl = 0; sl < NSL; ++sl)
+      if (exp_end(sl) - exp_begin(sl) > 2) return false;
+    return true;
+  }
   static constexpr bool slot_is_score(int sl) { return sl >= NMP; }
   // exponential pairs of slot sl: u with E0 + floor(u * (NSL - E0) / NEP) == sl
   static constexpr int exp_begin(int sl) { return sl < E0 ? 0 : ((sl - E0) * NEP + NSL - E0 - 1) / (NSL - E0); }
@@ -304,8 +326,11 @@ struct Attn {
     for (int i = 0; i < NMS; ++i) score_mfma(s, kf, sK, i);
   }
 
-  // Masked keys of tile n0 (key > i + diag, or key >= Sk) get mask_val.
+  // Masked keys of tile n0 (key > i + diag, or key >= Sk) get mask_val. The select is a bit
+  // select on the sign of (lim - key offset): a compare per element would need a scalar register
+  // pair per mask, and the scheduler hoists all 64 of them.
   __device__ __forceinline__ void mask_tile(Scores& s, int n0) const {
+    const uint32_t mv = __float_as_uint(mask_val);
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       const int row = qw + qb * 32 + i32;
@@ -314,8 +339,10 @@ struct Attn {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (kb * 32 + 16 * (r >> 3) + (r & 7) > lim) s[kb][qb][r] = mask_val;
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t m = (uint32_t)((lim - (kb * 32 + 16 * (r >> 3) + (r & 7))) >> 31);  // all ones if masked
+          s[kb][qb][r] = __uint_as_float((__float_as_uint(s[kb][qb][r]) & ~m) | (mv & m));
+        }
     }
   }
 
@@ -330,16 +357,26 @@ struct Attn {
   }
 
   // Exponential pair u of a tile: p = 2^(cs * s - m_ref), the lane's row sum, and the bf16 pair.
-  __device__ __forceinline__ void exp_pair(int u, const Scores& cur, Probs& pk, const float (&mref)[QB],
-                                           float (&rs)[QB]) const {
+  // In the step the pair is done in two halves in consecutive slots: exp_first (2 fma, 2 exp) and
+  // exp_second (2 add, 1 pack), which keeps every slot's VALU work below one MFMA.
+  __device__ __forceinline__ f32x2 exp_first(int u, const Scores& cur, const float (&mref)[QB]) const {
     const int qb = u % QB, rp = (u / QB) % 8, kb = u / (QB * 8);
-    const float e0 = __builtin_amdgcn_exp2f(fmaf(cur[kb][qb][2 * rp], cs, -mref[qb]));
-    const float e1 = __builtin_amdgcn_exp2f(fmaf(cur[kb][qb][2 * rp + 1], cs, -mref[qb]));
-    rs[qb] += e0 + e1;
-    pk[kb][qb][rp] = pack_bf16x2(e0, e1);
+    f32x2 e = {__builtin_amdgcn_exp2f(fmaf(cur[kb][qb][2 * rp], cs, -mref[qb])),
+               __builtin_amdgcn_exp2f(fmaf(cur[kb][qb][2 * rp + 1], cs, -mref[qb]))};
+    asm volatile("" : "+v"(e));
+    return e;
+  }
+  __device__ __forceinline__ void exp_second(int u, f32x2 e, Probs& pk, float (&rs)[QB]) const {
+    const int qb = u % QB, rp = (u / QB) % 8, kb = u / (QB * 8);
+    rs[qb] += e.x + e.y;
+    pk[kb][qb][rp] = pack_bf16x2(e.x, e.y);
     // Keep the pack here: otherwise it is sunk past the rebase branch, which keeps both fp32
     // exponentials alive across the whole step.
     asm volatile("" : "+v"(pk[kb][qb][rp]));
+  }
+  __device__ __forceinline__ void exp_pair(int u, const Scores& cur, Probs& pk, const float (&mref)[QB],
+                                           float (&rs)[QB]) const {
+    exp_second(u, exp_first(u, cur, mref), pk, rs);
   }
 
   // P V MFMA number p of a tile (order ps, db, qb), V fragments read VPF ahead.
@@ -416,6 +453,8 @@ struct Attn {
     bf16x8 vf[NVF];
 #pragma unroll
     for (int t = 0; t < VPF && t < NVF; ++t) vf[t] = vfrag(sVo, t / DB, t % DB);
+    static_assert(at_most_two_pairs_per_slot(), "ehalf holds the first halves of two slots");
+    f32x2 ehalf[4];  // first halves in flight
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
@@ -423,10 +462,17 @@ struct Attn {
         score_mfma(nxt, kf, sKn, sl - NMP);
       else
         pv_mfma(sl, pk_old, vf, sVo);
+      // second halves of the previous slot's pairs, first halves of this slot's pairs
+      if (sl > 0) {
 #pragma unroll
-      for (int u = exp_begin(sl); u < exp_end(sl); ++u) exp_pair(u, cur, pk_new, mref, rs);
+        for (int u = exp_begin(sl - 1); u < exp_end(sl - 1); ++u) exp_second(u, ehalf[u % 4], pk_new, rs);
+      }
+#pragma unroll
+      for (int u = exp_begin(sl); u < exp_end(sl); ++u) ehalf[u % 4] = exp_first(u, cur, mref);
       __builtin_amdgcn_sched_barrier(0);
     }
+#pragma unroll
+    for (int u = exp_begin(NSL - 1); u < exp_end(NSL - 1); ++u) exp_second(u, ehalf[u % 4], pk_new, rs);
     bool over = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) over = over || !(rs[qb] <= kOverflowSum);
@@ -481,6 +527,16 @@ void fa_fwd_kernel(FwdParams p) {
   }
   const int nt = (kv_end + BN - 1) / BN;
 
+  // Q rows of this wave as B operands of the score product, resident in AGPRs: lane (i32, h) holds
+  // row qw+32*qb+i32, dims 16*ks + 8*h .. +7. Rows past Sq read row Sq-1 instead; their outputs are
+  // never stored. Issued first, waited for together with the first K tile below.
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int row = min(st.qw + qb * 32 + st.i32, p.sq - 1);
+#pragma unroll
+    for (int ks = 0; ks < A::KS; ++ks) load_q(st.qf[qb][ks], qh + (size_t)row * DQK + ks * 16 + st.h * 8);
+  }
+
   // Rings: step j issues K(j+3) and V(j+2) (the group of step j); the prologue issues the groups of
   // j = -3, -2, -1, i.e. K0, K1, V0, K2, V1 in this order.
   TileLoader<C::NWAVES, BN, C::KCH> kload;
@@ -496,16 +552,19 @@ void fa_fwd_kernel(FwdParams p) {
   issue_group(-3);
   issue_group(-2);
   issue_group(-1);
-
-  // Q rows of this wave as B operands of the score product, resident in AGPRs: lane (i32, h) holds
-  // row qw+32*qb+i32, dims 16*ks + 8*h .. +7. Rows past Sq read row Sq-1 instead; their outputs are
-  // never stored. (load_q waits for all of this wave's loads, the prologue tiles included.)
+  // Q and K0 must have landed: the loads issued after K0 are K1, V0, K2, V1 (those that exist).
+  if (nt >= 3)
+    wait_vmcnt<2 * C::K_LOADS + 2 * C::V_LOADS>();
+  else if (nt == 2)
+    wait_vmcnt<C::K_LOADS + 2 * C::V_LOADS>();
+  else if (nt == 1)
+    wait_vmcnt<C::V_LOADS>();
+  else
+    wait_vmcnt<0>();
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int row = min(st.qw + qb * 32 + st.i32, p.sq - 1);
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int ks = 0; ks < A::KS; ++ks) st.qf[qb][ks] = load_q(qh + (size_t)row * DQK + ks * 16 + st.h * 8);
-  }
+    for (int ks = 0; ks < A::KS; ++ks) q_ready(st.qf[qb][ks]);
 
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -521,8 +580,9 @@ void fa_fwd_kernel(FwdParams p) {
   typename A::Scores sA, sB;
   typename A::Probs pA, pB;
   if (nt > 0) {
-    // Tile 0: scores, mask, exact row maxima. P of "tile -1" is zero (its P V step reads the
-    // finite V tile 0 and adds nothing).
+    // Tile 0: scores, mask, exact row maxima. P of "tile -1" is zero; its P V step reads a K slot
+    // that has landed and is not written during step 0 (K1, or K0 when it is the only tile): any
+    // finite data, times zero, adds nothing.
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
@@ -559,13 +619,13 @@ void fa_fwd_kernel(FwdParams p) {
   int j = 0;
   for (; j + 1 < nt; j += 2) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), vslot(j > 0 ? j - 1 : 0), j > 0 && j >= n_plain, j * BN);
+    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, j * BN);
     sync_step(j + 1);
     st.step(sB, sA, pB, pA, kslot(j + 2), vslot(j), j + 1 >= n_plain, (j + 1) * BN);
   }
   if (j < nt) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), vslot(j > 0 ? j - 1 : 0), j > 0 && j >= n_plain, j * BN);
+    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(0), j > 0 && j >= n_plain, j * BN);
   }
   if (nt > 0) {
     // P V of the last tile, on a selected copy of P: two calls would leave O in different
