@@ -198,10 +198,12 @@ struct TileLoader {
       voff[i] = (uint32_t)(row * CH + ((pch % CH) ^ swz(row))) * 16u;
     }
   }
-  // Buffer of the tile whose first row is key n0 (0 <= n0 < Sk), and this wave's LDS base in `slot`.
+  // Buffer of the tile whose first row is key n0 (n0 >= 0; a tile at or past Sk gets an empty
+  // buffer and loads zeros), and this wave's LDS base in `slot`.
   __device__ __forceinline__ u32x4 rsrc(int n0) const {
     const uint64_t base = head + (uint64_t)n0 * kRowBytes;
-    return u32x4{(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, (rows - (uint32_t)n0) * kRowBytes, 0x00020000u};
+    const uint32_t left = (int)rows > n0 ? (rows - (uint32_t)n0) * kRowBytes : 0u;
+    return u32x4{(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, left, 0x00020000u};
   }
   __device__ __forceinline__ uint32_t lds(unsigned char* slot, int wave) const {
     return lds_offset(slot + wave * NI * 1024);
@@ -209,7 +211,7 @@ struct TileLoader {
   __device__ __forceinline__ void issue_one(const u32x4& r, uint32_t l, int i) const {
     dma16_buffer(r, voff[i], l + i * 1024);
   }
-  // Issue all loads of the tile at key n0 into `slot`.
+  // Issue all loads of the tile at key n0 into `slot` at once.
   __device__ __forceinline__ void issue(int n0, unsigned char* slot, int wave) const {
     const u32x4 r = rsrc(n0);
     const uint32_t l = lds(slot, wave);
@@ -438,8 +440,12 @@ struct Attn {
 
   // One pipeline step: P V of tile j-1 (pk_old, V slot sVo), exponentials of tile j (cur, key n0,
   // into pk_new) and scores of tile j+1 (K slot sKn, into nxt).
+  // `issue(k)` starts load k (0 <= k < LOADS) of the tiles this step prefetches; the loads are spread
+  // one every NSL / LOADS slots, between MFMAs (a burst of them would stall the wave).
+  template <class Issue>
   __device__ __forceinline__ void step(Scores& cur, Scores& nxt, Probs& pk_new, const Probs& pk_old,
-                                       const unsigned char* sKn, const unsigned char* sVo, bool masked, int n0) {
+                                       const unsigned char* sKn, const unsigned char* sVo, bool masked, int n0,
+                                       Issue&& issue) {
     if (masked) mask_tile(cur, n0);
     float mref[QB], rs[QB];
 #pragma unroll
@@ -458,6 +464,11 @@ struct Attn {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
+      {
+        constexpr int NLD = C::K_LOADS + C::V_LOADS, SP = NSL / NLD;
+        static_assert(SP >= 1, "more loads than slots");
+        if (sl % SP == SP / 2 && sl / SP < NLD) issue(sl / SP);
+      }
       if (slot_is_score(sl))
         score_mfma(nxt, kf, sKn, sl - NMP);
       else
@@ -537,30 +548,23 @@ void fa_fwd_kernel(FwdParams p) {
     for (int ks = 0; ks < A::KS; ++ks) load_q(st.qf[qb][ks], qh + (size_t)row * DQK + ks * 16 + st.h * 8);
   }
 
-  // Rings: step j issues K(j+3) and V(j+2) (the group of step j); the prologue issues the groups of
-  // j = -3, -2, -1, i.e. K0, K1, V0, K2, V1 in this order.
+  // Rings: step j loads K(j+3) and V(j+2) (the group of step j); the prologue loads the groups of
+  // j = -3, -2, -1, i.e. K0, K1, V0, K2, V1 in this order. Every group is issued in full: a tile at
+  // or past the last one loads zeros into a slot nobody reads any more, so the number of loads
+  // issued after any given one is a constant and every wait below is a fixed count.
   TileLoader<C::NWAVES, BN, C::KCH> kload;
   TileLoader<C::NWAVES, BN, C::VCH> vload;
   kload.init(kh, p.sk, wave, lane, kswz);
   vload.init(vh, p.sk, wave, lane, vswz);
   auto kslot = [&](int t) { return smem + (t % C::NKR) * C::K_BYTES; };
   auto vslot = [&](int t) { return smem + C::NKR * C::K_BYTES + (t % C::NVR) * C::V_BYTES; };
-  auto issue_group = [&](int j) {
-    if (j + 3 < nt) kload.issue((j + 3) * BN, kslot(j + 3), wave);
-    if (j + 2 >= 0 && j + 2 < nt) vload.issue((j + 2) * BN, vslot(j + 2), wave);
-  };
-  issue_group(-3);
-  issue_group(-2);
-  issue_group(-1);
-  // Q and K0 must have landed: the loads issued after K0 are K1, V0, K2, V1 (those that exist).
-  if (nt >= 3)
-    wait_vmcnt<2 * C::K_LOADS + 2 * C::V_LOADS>();
-  else if (nt == 2)
-    wait_vmcnt<C::K_LOADS + 2 * C::V_LOADS>();
-  else if (nt == 1)
-    wait_vmcnt<C::V_LOADS>();
-  else
-    wait_vmcnt<0>();
+  kload.issue(0, kslot(0), wave);
+  kload.issue(BN, kslot(1), wave);
+  vload.issue(0, vslot(0), wave);
+  kload.issue(2 * BN, kslot(2), wave);
+  vload.issue(BN, vslot(1), wave);
+  // Q and K0 must have landed: K1, V0, K2, V1 were issued after K0.
+  wait_vmcnt<2 * C::K_LOADS + 2 * C::V_LOADS>();
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -580,9 +584,9 @@ void fa_fwd_kernel(FwdParams p) {
   typename A::Scores sA, sB;
   typename A::Probs pA, pB;
   if (nt > 0) {
-    // Tile 0: scores, mask, exact row maxima. P of "tile -1" is zero; its P V step reads a K slot
-    // that has landed and is not written during step 0 (K1, or K0 when it is the only tile): any
-    // finite data, times zero, adds nothing.
+    // Tile 0: scores, mask, exact row maxima. P of "tile -1" is zero; its P V step reads the K1
+    // slot, which has landed (or holds zeros) and is not written during step 0: finite data times
+    // zero adds nothing.
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
@@ -597,35 +601,38 @@ void fa_fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int r = 0; r < 8; ++r) pB[kb][qb][r] = 0u;
   }
-  // Before step j: K(j+1) and V(j-1) must have landed. This wave's loads issued after K(j+1) are
-  // V(j), K(j+2) (if it exists) and V(j+1); on the last step only V(j) follows V(j-1). The barrier
-  // then publishes every wave's part and guarantees that all waves are done with step j-1, whose
-  // slots (K(j), V(j-2)) the group of step j overwrites.
+  // Before step j: K(j+1) and V(j-1) must have landed; this wave's loads issued after K(j+1) are
+  // V(j), K(j+2) and V(j+1). The barrier then publishes every wave's part and guarantees that all
+  // waves are done with step j-1, whose slots (K(j), V(j-2)) the loads of step j overwrite.
+  u32x4 gk = {}, gv = {};
+  uint32_t gkl = 0, gvl = 0;
   auto sync_step = [&](int j) {
-    if (j + 1 < nt) {
-      if (j + 2 < nt)
-        wait_vmcnt<2 * C::V_LOADS + C::K_LOADS>();
-      else
-        wait_vmcnt<2 * C::V_LOADS>();
-    } else {
-      wait_vmcnt<C::V_LOADS>();
-    }
+    wait_vmcnt<2 * C::V_LOADS + C::K_LOADS>();
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    issue_group(j);
+    gk = kload.rsrc((j + 3) * BN);
+    gkl = kload.lds(kslot(j + 3), wave);
+    gv = vload.rsrc((j + 2) * BN);
+    gvl = vload.lds(vslot(j + 2), wave);
+  };
+  auto issue = [&](int k) {
+    if (k < C::K_LOADS)
+      kload.issue_one(gk, gkl, k);
+    else
+      vload.issue_one(gv, gvl, k - C::K_LOADS);
   };
   // Steps in pairs so that the two score tiles and the two P tiles swap roles without copies.
   int j = 0;
   for (; j + 1 < nt; j += 2) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, j * BN);
+    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, j * BN, issue);
     sync_step(j + 1);
-    st.step(sB, sA, pB, pA, kslot(j + 2), vslot(j), j + 1 >= n_plain, (j + 1) * BN);
+    st.step(sB, sA, pB, pA, kslot(j + 2), vslot(j), j + 1 >= n_plain, (j + 1) * BN, issue);
   }
   if (j < nt) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(0), j > 0 && j >= n_plain, j * BN);
+    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, j * BN, issue);
   }
   if (nt > 0) {
     // P V of the last tile, on a selected copy of P: two calls would leave O in different
@@ -646,6 +653,10 @@ void fa_fwd_kernel(FwdParams p) {
         for (int r = 0; r < 8; ++r) pl[kb][qb][r] = (pA[kb][qb][r] & take_a) | (pB[kb][qb][r] & ~take_a);
     st.pv_tile(pl, vslot(nt - 1));
   }
+
+  // No load may still be writing this workgroup's LDS when it exits (the prologue issues loads even
+  // when there is no key tile to visit).
+  wait_vmcnt<0>();
 
   // ---- epilogue: O = acc / l, LSE = ln 2 * (m + log2 l) ---------------------------------------
 #pragma unroll
