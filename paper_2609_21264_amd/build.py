@@ -30,9 +30,9 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: ROCm is required to build libfa.so")
 
 
-def compile_command(out: str, extra=()) -> list:
+def _device_flags() -> list:
     return [
-        hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+        f"--offload-arch={ARCH}", "-O3", "-std=c++17",
         # Packed fp32 VALU instructions are kept out of the generated code.
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         # Score MFMAs in VGPR form (the softmax reads them); the P V accumulators are pinned to
@@ -41,13 +41,29 @@ def compile_command(out: str, extra=()) -> list:
         # The pipelined step is one fully unrolled sequence of MFMA slots; the default limit for
         # "#pragma unroll" stops short of it for the widest head dimension.
         "-mllvm", "-pragma-unroll-threshold=50000",
-        "-Wall", "-Wno-unused-command-line-argument",
         "-I", INCLUDE, "-I", CSRC,
+    ]
+
+
+def compile_command(out: str, extra=()) -> list:
+    return [
+        hipcc(), *_device_flags(), "-fPIC", "-shared",
+        "-Wall", "-Wno-unused-command-line-argument",
         "-Wl,-rpath,/opt/rocm/lib",
         *extra,
         "-o", out,
         *[os.path.join(CSRC, s) for s in SOURCES],
     ]
+
+
+def kernel_asm(out: str) -> None:
+    """Write the gfx950 assembly of the kernel translation unit to `out` (for static checks of the
+    generated code; nothing is linked)."""
+    cmd = [hipcc(), *_device_flags(), "--cuda-device-only", "-S", "-w", "-o", out,
+           os.path.join(CSRC, "fa_fwd_kernel.hip")]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc -S failed:\n" + (res.stdout or "") + (res.stderr or ""))
 
 
 def build(verbose: bool = False, resource_usage: bool = False) -> str:

@@ -100,14 +100,19 @@ __device__ __forceinline__ float half_swap_sum(float x) {
 // The P V product is issued through inline asm so that its accumulators O stay in AGPRs for the
 // whole kernel (the score product uses the builtin; its accumulators are VGPRs). The compiler does
 // not model hazards of inline asm, so:
-//  * mfma_out starts with s_nop 1: its P operand may have just been written by VALU
-//    (v_cvt_pk_bf16_f32), which needs 2 wait states before an MFMA reads it;
+//  * mfma_out starts with s_nop 1: its P operand may have just been written by VALU, which needs
+//    2 wait states before an MFMA reads it (mfma_out_settled omits them where P is old);
 //  * agpr_fence() separates asm MFMA writes of O from compiler-generated accesses (initialisation,
 //    rescale, epilogue) in both directions: 18 wait states cover the MFMA write-to-read distance,
 //    and the operand tie keeps the order;
 //  * consecutive MFMAs accumulating into exactly the same registers need no wait states.
 __device__ __forceinline__ void mfma_out(f32x16& acc, const bf16x8& v, const bf16x8& pt) {
   asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(pt));
+}
+// Same without the leading wait states, for operands no VALU instruction has written recently: in
+// the pipelined step, P was packed a whole step earlier and V comes from LDS.
+__device__ __forceinline__ void mfma_out_settled(f32x16& acc, const bf16x8& v, const bf16x8& pt) {
+  asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(pt));
 }
 __device__ __forceinline__ void agpr_fence(f32x16& acc) {
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+a"(acc));
@@ -381,13 +386,18 @@ struct Attn {
     exp_second(u, exp_first(u, cur, mref), pk, rs);
   }
 
-  // P V MFMA number p of a tile (order ps, db, qb), V fragments read VPF ahead.
-  __device__ __forceinline__ void pv_mfma(int p, const Probs& pk, bf16x8 (&vf)[NVF], const unsigned char* sV) {
+  // P V MFMA number p of a tile (order ps, db, qb), V fragments read VPF ahead. `settled`: P was
+  // written long before (in the step: one step earlier), so no wait states are needed.
+  __device__ __forceinline__ void pv_mfma(int p, const Probs& pk, bf16x8 (&vf)[NVF], const unsigned char* sV,
+                                          bool settled = false) {
     const int t = p / QB, qb = p % QB, ps = t / DB, db = t % DB;
     if (qb == 0 && t + VPF < NVF) vf[t + VPF] = vfrag(sV, (t + VPF) / DB, (t + VPF) % DB);
     const int kb = ps >> 1, base = (ps & 1) * 4;
     const u32x4 w = {pk[kb][qb][base], pk[kb][qb][base + 1], pk[kb][qb][base + 2], pk[kb][qb][base + 3]};
-    mfma_out(oacc[db][qb], vf[t], bit_cast<bf16x8>(w));
+    if (settled)
+      mfma_out_settled(oacc[db][qb], vf[t], bit_cast<bf16x8>(w));
+    else
+      mfma_out(oacc[db][qb], vf[t], bit_cast<bf16x8>(w));
   }
 
   // All P V MFMAs of one tile (the last tile, after the loop).
@@ -472,7 +482,7 @@ struct Attn {
       if (slot_is_score(sl))
         score_mfma(nxt, kf, sKn, sl - NMP);
       else
-        pv_mfma(sl, pk_old, vf, sVo);
+        pv_mfma(sl, pk_old, vf, sVo, true);
       // second halves of the previous slot's pairs, first halves of this slot's pairs
       if (sl > 0) {
 #pragma unroll
