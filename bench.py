@@ -126,8 +126,11 @@ def parity_sample(w, q, k, v, o, lse, rows_per_head: int = 4):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=-1,
+                    help="timed steps; default: at least 20 and at least 0.25 s of launches")
+    ap.add_argument("--warmup", type=int, default=-1,
+                    help="untimed steps first; default: at least 10 and at least 0.5 s (the first tens of "
+                         "milliseconds of back-to-back launches run slower while clocks and caches settle)")
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -163,10 +166,29 @@ def main():
         if st != 0:
             raise fa.FaError(st)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    step_s = None  # wall time per step seen during warmup
+    if args.warmup >= 0:
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+    else:
+        # Warm up for a fixed time rather than a fixed count; the count done is what is reported.
+        args.warmup = 0
+        t_w = time.perf_counter()
+        while args.warmup < 10 or time.perf_counter() - t_w < 0.5:
+            for _ in range(max(1, min(64, args.warmup))):
+                step()
+                args.warmup += 1
+            torch.cuda.synchronize()
+        step_s = (time.perf_counter() - t_w) / args.warmup
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    if args.steps < 0:
+        if step_s is None:
+            t_p = time.perf_counter()
+            step()
+            torch.cuda.synchronize()
+            step_s = time.perf_counter() - t_p
+        args.steps = max(20, int(0.25 / max(step_s, 1e-6)) + 1)
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()

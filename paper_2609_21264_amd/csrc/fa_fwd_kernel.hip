@@ -26,9 +26,9 @@
 //    slots, step j loads V(j+2)). One wait on the wave's own loads plus one barrier per step
 //    publishes the tiles of the step and frees the slots of the previous one. Rows past Sk load as
 //    zeros (buffer range check), so partial tiles need no special path.
-//  * 16-byte LDS chunks are XOR-swizzled per row (K: by the reading lane's key slot; V: by
-//    2*(key mod 4)) so that the lanes served together hit different banks. The swizzle is produced
-//    by choosing each lane's source offset, since the load writes LDS lane-linearly.
+//  * 16-byte LDS chunks are XOR-swizzled per row (K: by the reading lane's key slot; V: by the key
+//    mod 4) so that the lanes the LDS serves in one cycle hit 16 different bank slots. The swizzle
+//    is produced by choosing each lane's source offset, since the load writes LDS lane-linearly.
 //  * The output accumulators O and the Q operand live in AGPRs for the whole kernel; scores,
 //    probabilities and LDS fragments use VGPRs.
 //  * Causal masking skips key tiles above the diagonal entirely and applies the element mask only on
@@ -57,7 +57,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 #define FA_KPF 2
 #endif
 #ifndef FA_VPF
-#define FA_VPF 4
+#define FA_VPF 6
 #endif
 
 constexpr float kLn2 = 0.69314718055994530942f;
@@ -71,13 +71,36 @@ constexpr int kNumXcd = 8;
 // 8*(r/4) + 4*h + r%4), register r then holds key 16*(r/8) + 8*h + r%8.
 __device__ __forceinline__ int perm32(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
 
-// XOR swizzle of the 16-byte chunks of K-tile row `row`. The reading lanes 0..7 of a phase load
-// rows perm32(0..7) (+32*kb), whose swizzles are 0..7.
-__device__ __forceinline__ int k_swizzle(int row) { return perm32(row & 31) & 7; }
+// LDS on gfx950 has 64 four-byte banks (256 bytes per cycle). A ds_read_b128 is served 16 lanes per
+// cycle and a ds_read_b64_tr_b16 32 lanes per cycle; the lanes served together must touch 16
+// different 16-byte bank slots to avoid conflicts.
+//
+// XOR swizzle of the 16-byte chunks of K-tile row `row`, as a function of the reading lane
+// i = perm32(row % 32) (lanes 16m..16m+15 of a K fragment read rows perm32(i) of one chunk column).
+// DQK = 128 (16 chunks per row, every row starts at bank 0): a 4-bit XOR by i. DQK = 64 or 192 (rows
+// start alternately at bank 0 and 32, i.e. row parity = i parity selects the half): a 3-bit XOR by
+// i / 2, which stays inside each aligned group of 8 chunks.
+template <int DQK>
+__device__ __forceinline__ int k_lane_swizzle(int i) { return (DQK / 8) % 16 == 0 ? (i & 15) : ((i >> 1) & 7); }
+template <int DQK>
+__device__ __forceinline__ int k_swizzle(int row) { return k_lane_swizzle<DQK>(perm32(row & 31)); }
 
-// XOR swizzle of the 16-byte chunks of V-tile row `key`: the four key rows a 16-lane group of the
-// transpose read touches at once land in different 32-byte bank slots.
-__device__ __forceinline__ int v_swizzle(int key) { return 2 * (key & 3); }
+// XOR swizzle of the 16-byte chunks of V-tile row `key`. Lanes 0..31 of the transpose read touch
+// keys k..k+3 (k a multiple of 4), 64 bytes each, at the same chunk columns: DV = 128 spreads the
+// four rows over chunk bits 2..3 (every row starts at bank 0); DV = 64 over bits 1..2 (there row
+// parity already separates bank halves).
+template <int DV>
+__device__ __forceinline__ int v_swizzle(int key) { return DV >= 128 ? 4 * (key & 3) : 2 * (key & 3); }
+
+// Layout of the output tile staged in LDS for coalesced stores: row R of a wave's tile (DV bf16,
+// 16-byte chunks) keeps logical chunk c at chunk c ^ o_swizzle(R), with the chunk's two 8-byte
+// halves exchanged when o_half(R) = 1. The accumulator layout writes 8 bytes per lane for 32 rows at
+// once and the coalesced read takes 8 bytes per lane across consecutive rows; with this layout both
+// touch 32 different 8-byte bank slots per cycle.
+template <int DV>
+__device__ __forceinline__ int o_swizzle(int r) { return DV >= 128 ? (r & 15) : ((r >> 1) & 7); }
+template <int DV>
+__device__ __forceinline__ int o_half(int r) { return DV >= 128 ? ((r ^ (r >> 4)) & 1) : (((r >> 1) ^ (r >> 4)) & 1); }
 
 template <class T, class U>
 __device__ __forceinline__ T bit_cast(const U& u) {
@@ -182,20 +205,22 @@ struct Cfg {
 // This wave's share of the direct-to-LDS loads of one K or V tile (BN rows of CH 16-byte chunks).
 // Physical chunk p of a slot holds logical chunk (p % CH) ^ swz(row) of row p / CH, so the lanes'
 // source offsets carry the swizzle; they are computed once. Each tile is described by a buffer
-// whose base is the tile's first row and whose size ends at row Sk: rows past Sk load as zeros
-// (their scores are masked and their V rows meet P = 0). One head's K or V spans less than 4 GiB
-// (the API bounds Sk * d), so 32-bit record counts suffice.
+// whose base is the tile's first row and whose size ends at the workgroup's last visible key
+// (Sk, or the causal limit of its last query row): rows past it load as zeros without a memory
+// access (their scores are masked and their V rows meet P = 0), which also makes the loads of tiles
+// past the last one cheap. One head's K or V spans less than 4 GiB (the API bounds Sk * d), so
+// 32-bit record counts suffice.
 template <int NWAVES, int BN, int CH>
 struct TileLoader {
   static constexpr int NI = BN * CH / 64 / NWAVES;  // loads per wave per tile
   static constexpr uint32_t kRowBytes = CH * 16;
   uint64_t head;      // first row of this head (wave-uniform)
-  uint32_t rows;      // Sk
+  uint32_t rows;      // keys visible to the workgroup
   uint32_t voff[NI];  // bytes from the tile's first row
   template <class Swz>
-  __device__ __forceinline__ void init(const uint16_t* head_, int sk, int wave, int lane, Swz swz) {
+  __device__ __forceinline__ void init(const uint16_t* head_, int nrows, int wave, int lane, Swz swz) {
     head = reinterpret_cast<uint64_t>(head_);
-    rows = (uint32_t)sk;
+    rows = (uint32_t)nrows;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int pch = (wave * NI + i) * 64 + lane;
@@ -306,7 +331,7 @@ struct Attn {
 
   __device__ __forceinline__ u32x4 kfrag(const unsigned char* sK, int ks, int kb) const {
     const int row = kb * 32 + perm32(i32);
-    return *reinterpret_cast<const u32x4*>(sK + row * (DQK * 2) + (((ks * 2 + h) ^ (i32 & 7)) << 4));
+    return *reinterpret_cast<const u32x4*>(sK + row * (DQK * 2) + (((ks * 2 + h) ^ k_lane_swizzle<DQK>(i32)) << 4));
   }
   // A operand V^T[dims db*32 + 0..31][keys 16*ps + 0..15]: lane (group G, slot j) points the
   // transpose read at key 16*ps + 8*(G/2) + j/4 (then +4), dims db*32 + 16*(G%2) + 4*(j%4).
@@ -510,8 +535,8 @@ void fa_fwd_kernel(FwdParams p) {
   constexpr int DQK = C::DQK, DV = C::DV, BN = C::BN, QB = C::QB;
 
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS_BYTES];
-  auto kswz = [](int row) { return k_swizzle(row); };
-  auto vswz = [](int row) { return v_swizzle(row); };
+  auto kswz = [](int row) { return k_swizzle<DQK>(row); };
+  auto vswz = [](int row) { return v_swizzle<DV>(row); };
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -520,7 +545,7 @@ void fa_fwd_kernel(FwdParams p) {
   st.h = lane >> 5;
   // Lane constants of the V transpose read: group G = lane/16, slot j = lane%16.
   st.v_key = 8 * (lane >> 5) + ((lane & 15) >> 2);                             // key in the 16-key step
-  st.v_t = (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) ^ v_swizzle(st.v_key);  // low chunk bits, swizzled
+  st.v_t = (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) ^ v_swizzle<DV>(st.v_key);  // low chunk bits, swizzled
   st.v_half = (lane & 1) * 8;                                                  // byte offset in the chunk
   st.cs = p.cs;
   st.mask_val = p.cs < 0.f ? INFINITY : -INFINITY;
@@ -564,8 +589,8 @@ void fa_fwd_kernel(FwdParams p) {
   // issued after any given one is a constant and every wait below is a fixed count.
   TileLoader<C::NWAVES, BN, C::KCH> kload;
   TileLoader<C::NWAVES, BN, C::VCH> vload;
-  kload.init(kh, p.sk, wave, lane, kswz);
-  vload.init(vh, p.sk, wave, lane, vswz);
+  kload.init(kh, kv_end, wave, lane, kswz);
+  vload.init(vh, kv_end, wave, lane, vswz);
   auto kslot = [&](int t) { return smem + (t % C::NKR) * C::K_BYTES; };
   auto vslot = [&](int t) { return smem + C::NKR * C::K_BYTES + (t % C::NVR) * C::V_BYTES; };
   kload.issue(0, kslot(0), wave);
@@ -648,8 +673,9 @@ void fa_fwd_kernel(FwdParams p) {
     // P V of the last tile, on a selected copy of P: two calls would leave O in different
     // registers and the copies that merge them could read MFMA results before they are written.
     // (The select is a bit mask: a ternary on the elements would be folded into a select of the
-    // two arrays' addresses, which forces both into scratch memory.)
-    wait_vmcnt<0>();
+    // two arrays' addresses, which forces both into scratch memory.) V(nt-1) belongs to the load
+    // group of step nt-3; the groups of steps nt-2 and nt-1 may still be in flight.
+    wait_vmcnt<2 * (C::K_LOADS + C::V_LOADS)>();
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
@@ -665,33 +691,72 @@ void fa_fwd_kernel(FwdParams p) {
   }
 
   // No load may still be writing this workgroup's LDS when it exits (the prologue issues loads even
-  // when there is no key tile to visit).
+  // when there is no key tile to visit), and the output tile is staged in the ring slots below: every
+  // wave's loads must have landed and every wave must be done with the last V tile.
   wait_vmcnt<0>();
+  compiler_fence();
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
 
   // ---- epilogue: O = acc / l, LSE = ln 2 * (m + log2 l) ---------------------------------------
+  // O goes through LDS so that each store instruction writes whole rows (1 KiB contiguous); stored
+  // straight from the accumulator layout, every instruction would touch 32 rows 16 bytes at a time.
+  constexpr int RB = DV * 2;           // bytes per output row
+  constexpr int WROWS = 32 * QB;       // rows per wave
+  static_assert(C::NWAVES * WROWS * RB <= C::LDS_BYTES, "output staging fits in the ring slots");
+  unsigned char* stage = smem + wave * WROWS * RB;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
     for (int db = 0; db < A::DB; ++db) agpr_fence(st.oacc[db][qb]);
+  {
+    const int osw = o_swizzle<DV>(st.i32) << 4;             // qb * 32 leaves the low 5 row bits alone
+    const int ohalf = (st.h ^ o_half<DV>(st.i32)) << 3;
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const float l_tot = half_swap_sum(st.l_run[qb]);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const int row = st.qw + qb * 32 + st.i32;
-    if (row < p.sq) {
-      uint16_t* orow = p.o + ((size_t)(b * p.hq + hq) * p.sq + row) * DV;
+    for (int qb = 0; qb < QB; ++qb) {
+      const float l_tot = half_swap_sum(st.l_run[qb]);
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      unsigned char* srow = stage + (qb * 32 + st.i32) * RB + ohalf;
 #pragma unroll
       for (int db = 0; db < A::DB; ++db)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
-          const int d = db * 32 + 8 * g4 + 4 * st.h;
+          const int c = 4 * db + g4;  // 16-byte chunk: dims 8c .. 8c+7, this lane's half 4h .. 4h+3
           const uint32_t w0 = pack_bf16x2(st.oacc[db][qb][4 * g4] * inv, st.oacc[db][qb][4 * g4 + 1] * inv);
           const uint32_t w1 = pack_bf16x2(st.oacc[db][qb][4 * g4 + 2] * inv, st.oacc[db][qb][4 * g4 + 3] * inv);
-          *reinterpret_cast<uint2*>(orow + d) = make_uint2(w0, w1);
+          *reinterpret_cast<uint2*>(srow + ((c << 4) ^ osw)) = make_uint2(w0, w1);
         }
-      if (p.lse != nullptr && st.h == 0)
+      const int row = st.qw + qb * 32 + st.i32;
+      if (p.lse != nullptr && st.h == 0 && row < p.sq)
         p.lse[(size_t)(b * p.hq + hq) * p.sq + row] =
             l_tot > 0.f ? (st.m_run[qb] + log2f(l_tot)) * kLn2 : -INFINITY;
+    }
+  }
+  // Each wave reads back only its own rows, so no barrier: LDS serves one wave's accesses in order.
+  {
+    constexpr int CPR = RB / 16;        // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;       // rows per store instruction
+    const int c = lane % CPR;
+    uint16_t* ohead = p.o + (size_t)(b * p.hq + hq) * p.sq * DV;
+    // All reads first, pinned before the stores as a group: the compiler would otherwise sink each
+    // read into its store's row guard and wait out an LDS round trip per store.
+    constexpr int NIT = WROWS / RPI;
+    u32x4 ov[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int r = it * RPI + lane / CPR;
+      const unsigned char* chunk = stage + r * RB + ((c ^ o_swizzle<DV>(r)) << 4);
+      const int hl = o_half<DV>(r) << 3;
+      const uint2 x = *reinterpret_cast<const uint2*>(chunk + hl);
+      const uint2 y = *reinterpret_cast<const uint2*>(chunk + (hl ^ 8));
+      ov[it] = u32x4{x.x, x.y, y.x, y.y};
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) asm volatile("" : "+v"(ov[it]));
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int row = st.qw + it * RPI + lane / CPR;
+      if (row < p.sq) *reinterpret_cast<u32x4*>(ohead + (size_t)row * DV + c * 8) = ov[it];
     }
   }
 }
