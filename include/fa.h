@@ -45,6 +45,8 @@
 #ifndef FA_MI355X_FA_H
 #define FA_MI355X_FA_H
 
+#include <stddef.h>
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -58,7 +60,9 @@ typedef enum {
   FA_ERR_UNSUPPORTED = 3,  /* (d_qk, d_v) not compiled in; Q/K/V/O not 16-byte aligned, or LSE   */
                            /* not 4-byte aligned                                                  */
   FA_ERR_BAD_SCALE = 4,    /* scale is NaN or +-inf, or |scale| * log2(e) overflows float32       */
-  FA_ERR_HIP = 5           /* the HIP runtime reported an error when enqueuing the kernel         */
+  FA_ERR_HIP = 5,          /* the HIP runtime reported an error when enqueuing the kernel         */
+  FA_ERR_WORKSPACE = 6     /* split mode: workspace NULL or smaller than                          */
+                           /* fa_fwd_split_workspace_bytes(B, Hq, Sq, d_v, n_split)               */
 } fa_status_t;
 
 /*
@@ -83,6 +87,39 @@ fa_status_t fa_fwd(const void* Q, const void* K, const void* V, void* O, int B, 
 fa_status_t fa_fwd_ex(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
                       int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
                       void* stream);
+
+/*
+ * fa_fwd_split -- the same operation with every query block's key range cut into n_split parts that
+ * run as separate workgroups, for shapes with too few query blocks to fill the GPU (short or few
+ * query rows against long keys). This is the paper's tile-to-tile level (Alg. 2, Sec. 2.1): each
+ * part runs the per-tile online softmax (Alg. 1) over its contiguous run of 64-key tiles and yields a
+ * partial result; a second kernel merges the parts of every row with the log-sum-exp combination
+ * (u = max over parts of u_c; each part's accumulator and row sum rescaled by exp(u_c - u) before
+ * they are added), then normalises. Results agree with fa_fwd_ex within floating-point rounding.
+ *
+ *   Q .. stream  as in fa_fwd_ex
+ *   n_split      parts per query block (>= 1). Each query block's visible key tiles are divided into
+ *                n_split runs of ceil(tiles / n_split) tiles; parts left without a tile contribute
+ *                nothing.
+ *   workspace    device buffer owned by the caller, 16-byte aligned, at least
+ *                fa_fwd_split_workspace_bytes(B, Hq, Sq, d_v, n_split) bytes; overwritten by the call
+ *                (fp32 partial outputs [n_split][B][Hq][Sq][d_v], then partial LSE
+ *                [n_split][B][Hq][Sq]); the caller must not touch it until the call's work on
+ *                `stream` has completed. NULL is allowed only when no byte is needed.
+ *   workspace_bytes  its size in bytes
+ *
+ * Enqueues two kernels on `stream`. Errors: n_split < 1 first (FA_ERR_BAD_SHAPE), then the checks of
+ * fa_fwd_ex in their order (a degenerate size still returns FA_OK without touching the workspace),
+ * then more than 2^31-1 workgroups in total (FA_ERR_BAD_SHAPE), workspace NULL or too small
+ * (FA_ERR_WORKSPACE), workspace not 16-byte aligned (FA_ERR_UNSUPPORTED).
+ */
+fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
+                         int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
+                         int n_split, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes fa_fwd_split needs: n_split * B * Hq * Sq * (d_v + 1) * 4; 0 when B, Hq, Sq, d_v
+ * or n_split is <= 0 (nothing to store); SIZE_MAX if the count overflows. */
+size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split);
 
 /* Static, human-readable name of a status code ("FA_OK", ...); "unknown status" otherwise. */
 const char* fa_status_str(fa_status_t s);

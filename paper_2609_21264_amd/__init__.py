@@ -4,9 +4,11 @@ A thin Python binding over ``libfa.so``, whose C ABI is declared in ``include/fa
 supplies device memory and the stream; every step of the computation runs in the library's HIP
 kernel. The functions below marshal arguments and translate status codes, nothing more.
 
-* :func:`fa_fwd`, :func:`fa_fwd_ex`, :func:`fa_status_str`, :func:`fa_block_rows` -- the C entry
-  points under the same names, taking raw device pointers (ints) and sizes.
-* :func:`forward` -- convenience wrapper over torch tensors.
+* :func:`fa_fwd`, :func:`fa_fwd_ex`, :func:`fa_fwd_split`, :func:`fa_fwd_split_workspace_bytes`,
+  :func:`fa_status_str`, :func:`fa_block_rows` -- the C entry points under the same names, taking raw
+  device pointers (ints) and sizes.
+* :func:`forward` -- convenience wrapper over torch tensors (``n_split`` > 1 selects split mode and
+  takes the workspace from torch's allocator).
 """
 
 from __future__ import annotations
@@ -16,9 +18,10 @@ from typing import Optional
 
 from . import _lib
 from ._lib import (FA_ERR_BAD_SCALE, FA_ERR_BAD_SHAPE, FA_ERR_HIP, FA_ERR_NULL_POINTER,  # noqa: F401
-                   FA_ERR_UNSUPPORTED, FA_OK, LIB_PATH)
+                   FA_ERR_UNSUPPORTED, FA_ERR_WORKSPACE, FA_OK, LIB_PATH)
 
-__all__ = ["fa_fwd", "fa_fwd_ex", "fa_status_str", "fa_block_rows", "forward", "FaError", "LIB_PATH"]
+__all__ = ["fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_status_str",
+           "fa_block_rows", "forward", "FaError", "LIB_PATH"]
 
 
 class FaError(RuntimeError):
@@ -50,14 +53,28 @@ def fa_fwd_ex(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, Hq: in
                                      int(bool(causal)), stream))
 
 
+def fa_fwd_split(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, Hq: int, Hkv: int, Sq: int,
+                 Sk: int, d_qk: int, d_v: int, scale: float, causal: bool, n_split: int, workspace: Optional[int],
+                 workspace_bytes: int, stream: int) -> int:
+    """C ``fa_fwd_split``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_fwd_split(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, float(scale),
+                                        int(bool(causal)), int(n_split), workspace, int(workspace_bytes), stream))
+
+
+def fa_fwd_split_workspace_bytes(B: int, Hq: int, Sq: int, d_v: int, n_split: int) -> int:
+    """C ``fa_fwd_split_workspace_bytes``."""
+    return int(_lib.load().fa_fwd_split_workspace_bytes(int(B), int(Hq), int(Sq), int(d_v), int(n_split)))
+
+
 def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return_lse: bool = False,
-            out=None, lse=None, stream=None):
+            out=None, lse=None, stream=None, n_split: int = 1):
     """Attention forward over contiguous bf16 BHSD torch tensors on one GPU.
 
     q [B, Hq, Sq, d_qk], k [B, Hkv, Sk, d_qk], v [B, Hkv, Sk, d_v]; returns O [B, Hq, Sq, d_v] (bf16)
     and, with ``return_lse``, LSE [B, Hq, Sq] (float32, natural log). ``scale`` defaults to
-    1/sqrt(d_qk). The kernel is enqueued on ``stream`` (default: torch's current stream); the call
-    does not synchronise.
+    1/sqrt(d_qk). ``n_split`` > 1 runs split mode (``fa_fwd_split``) with that many key-range parts
+    per query block and a workspace from torch's allocator. The kernels are enqueued on ``stream``
+    (default: torch's current stream); the call does not synchronise.
     """
     import torch
 
@@ -90,12 +107,23 @@ def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
     handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    name = "fa_fwd_ex"
     with torch.cuda.device(q.device):
-        st = fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                       lse.data_ptr() if lse is not None else None,
-                       B, Hq, Hkv, Sq, Sk, dqk, dv, scale, causal, handle)
+        if n_split is not None and int(n_split) > 1:
+            name = "fa_fwd_split"
+            nbytes = fa_fwd_split_workspace_bytes(B, Hq, Sq, dv, int(n_split))
+            ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+            if isinstance(stream, torch.cuda.Stream):
+                ws.record_stream(stream)  # the caching allocator must not reuse it before the kernels ran
+            st = fa_fwd_split(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                              lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, dqk, dv, scale,
+                              causal, int(n_split), ws.data_ptr(), nbytes, handle)
+        else:
+            st = fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                           lse.data_ptr() if lse is not None else None,
+                           B, Hq, Hkv, Sq, Sk, dqk, dv, scale, causal, handle)
     if st != FA_OK:
-        if st in (FA_ERR_NULL_POINTER, FA_ERR_BAD_SHAPE, FA_ERR_UNSUPPORTED, FA_ERR_BAD_SCALE):
-            raise ValueError(f"fa_fwd_ex rejected the arguments: {fa_status_str(st)}")
+        if st in (FA_ERR_NULL_POINTER, FA_ERR_BAD_SHAPE, FA_ERR_UNSUPPORTED, FA_ERR_BAD_SCALE, FA_ERR_WORKSPACE):
+            raise ValueError(f"{name} rejected the arguments: {fa_status_str(st)}")
         raise FaError(st)
     return (out, lse) if return_lse else out

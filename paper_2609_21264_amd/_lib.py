@@ -19,9 +19,11 @@ FA_ERR_BAD_SHAPE = 2
 FA_ERR_UNSUPPORTED = 3
 FA_ERR_BAD_SCALE = 4
 FA_ERR_HIP = 5
+FA_ERR_WORKSPACE = 6
 
 #: Symbols include/fa.h declares.
-EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_status_str", "fa_block_rows")
+EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_status_str",
+            "fa_block_rows")
 
 _lib = None
 
@@ -42,6 +44,10 @@ def load() -> ctypes.CDLL:
     lib.fa_fwd.restype = i
     lib.fa_fwd_ex.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, vp]
     lib.fa_fwd_ex.restype = i
+    lib.fa_fwd_split.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, i, vp, ctypes.c_size_t, vp]
+    lib.fa_fwd_split.restype = i
+    lib.fa_fwd_split_workspace_bytes.argtypes = [i, i, i, i, i]
+    lib.fa_fwd_split_workspace_bytes.restype = ctypes.c_size_t
     lib.fa_status_str.argtypes = [i]
     lib.fa_status_str.restype = ctypes.c_char_p
     lib.fa_block_rows.argtypes = [i, i, i]

@@ -49,6 +49,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -180,10 +181,13 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
 // Compiler-level memory fence (no instruction): keeps LDS reads on their side of a barrier.
 __device__ __forceinline__ void compiler_fence() { asm volatile("" : : : "memory"); }
 
-template <int DQK_, int DV_, int BN_, int NWAVES_, int QB_, bool CAUSAL_>
+template <int DQK_, int DV_, int BN_, int NWAVES_, int QB_, bool CAUSAL_, bool SPLIT_>
 struct Cfg {
   static constexpr int DQK = DQK_, DV = DV_, BN = BN_, NWAVES = NWAVES_, QB = QB_;
   static constexpr bool CAUSAL = CAUSAL_;
+  // SPLIT: each workgroup takes one of n_split contiguous parts of its query block's key tiles and
+  // writes a partial result (O normalised by its own row sum, fp32, and its LSE) for a merge pass.
+  static constexpr bool SPLIT = SPLIT_;
   static constexpr int NT = NWAVES * 64;
   static constexpr int BM = NWAVES * 32 * QB;  // query rows per workgroup
   static constexpr int KCH = DQK / 8;          // 16-byte chunks per K-tile row
@@ -551,8 +555,10 @@ void fa_fwd_kernel(FwdParams p) {
   st.mask_val = p.cs < 0.f ? INFINITY : -INFINITY;
   st.sk = p.sk;
 
+  // Split mode: workgroup t takes part t / n_wg of work item t % n_wg.
+  const int split = C::SPLIT ? (int)(blockIdx.x / p.n_wg) : 0;
   int b, hq, qtile;
-  decode_workgroup(blockIdx.x, p, C::CAUSAL, b, hq, qtile);
+  decode_workgroup(C::SPLIT ? (int)(blockIdx.x % p.n_wg) : (int)blockIdx.x, p, C::CAUSAL, b, hq, qtile);
   const int g = hq / p.group;
   const uint16_t* __restrict__ qh = p.q + (size_t)(b * p.hq + hq) * p.sq * DQK;
   const uint16_t* __restrict__ kh = p.k + (size_t)(b * p.hkv + g) * p.sk * DQK;
@@ -571,7 +577,16 @@ void fa_fwd_kernel(FwdParams p) {
     kv_end = max(0, min(p.sk, last_row + st.diag + 1));
     n_plain = min(n_plain, max(0, q0 + st.diag + 1) / BN);
   }
-  const int nt = (kv_end + BN - 1) / BN;
+  // Key tiles [t0, t0 + nt) of the query block: all of them, or one contiguous part in split mode.
+  int t0 = 0, nt = (kv_end + BN - 1) / BN;
+  if (C::SPLIT) {
+    const int per = (nt + p.n_split - 1) / p.n_split;
+    t0 = min(nt, split * per);
+    nt = min(nt, t0 + per) - t0;
+  }
+  const int kb0 = t0 * BN;                     // first key of the range
+  n_plain = min(max(n_plain - t0, 0), nt);     // leading tiles of the range that need no mask
+  const int kv_lim = min(kv_end, kb0 + nt * BN);  // keys loaded; past it the tile loads read zeros
 
   // Q rows of this wave as B operands of the score product, resident in AGPRs: lane (i32, h) holds
   // row qw+32*qb+i32, dims 16*ks + 8*h .. +7. Rows past Sq read row Sq-1 instead; their outputs are
@@ -589,15 +604,15 @@ void fa_fwd_kernel(FwdParams p) {
   // issued after any given one is a constant and every wait below is a fixed count.
   TileLoader<C::NWAVES, BN, C::KCH> kload;
   TileLoader<C::NWAVES, BN, C::VCH> vload;
-  kload.init(kh, kv_end, wave, lane, kswz);
-  vload.init(vh, kv_end, wave, lane, vswz);
+  kload.init(kh, kv_lim, wave, lane, kswz);
+  vload.init(vh, kv_lim, wave, lane, vswz);
   auto kslot = [&](int t) { return smem + (t % C::NKR) * C::K_BYTES; };
   auto vslot = [&](int t) { return smem + C::NKR * C::K_BYTES + (t % C::NVR) * C::V_BYTES; };
-  kload.issue(0, kslot(0), wave);
-  kload.issue(BN, kslot(1), wave);
-  vload.issue(0, vslot(0), wave);
-  kload.issue(2 * BN, kslot(2), wave);
-  vload.issue(BN, vslot(1), wave);
+  kload.issue(kb0, kslot(0), wave);
+  kload.issue(kb0 + BN, kslot(1), wave);
+  vload.issue(kb0, vslot(0), wave);
+  kload.issue(kb0 + 2 * BN, kslot(2), wave);
+  vload.issue(kb0 + BN, vslot(1), wave);
   // Q and K0 must have landed: K1, V0, K2, V1 were issued after K0.
   wait_vmcnt<2 * C::K_LOADS + 2 * C::V_LOADS>();
 #pragma unroll
@@ -626,7 +641,7 @@ void fa_fwd_kernel(FwdParams p) {
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     st.scores(sA, kslot(0));
-    if (n_plain == 0) st.mask_tile(sA, 0);
+    if (n_plain == 0) st.mask_tile(sA, kb0);
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) st.m_run[qb] = st.row_max(sA, qb);
 #pragma unroll
@@ -646,9 +661,9 @@ void fa_fwd_kernel(FwdParams p) {
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    gk = kload.rsrc((j + 3) * BN);
+    gk = kload.rsrc(kb0 + (j + 3) * BN);
     gkl = kload.lds(kslot(j + 3), wave);
-    gv = vload.rsrc((j + 2) * BN);
+    gv = vload.rsrc(kb0 + (j + 2) * BN);
     gvl = vload.lds(vslot(j + 2), wave);
   };
   auto issue = [&](int k) {
@@ -661,13 +676,15 @@ void fa_fwd_kernel(FwdParams p) {
   int j = 0;
   for (; j + 1 < nt; j += 2) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, j * BN, issue);
+    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, kb0 + j * BN,
+            issue);
     sync_step(j + 1);
-    st.step(sB, sA, pB, pA, kslot(j + 2), vslot(j), j + 1 >= n_plain, (j + 1) * BN, issue);
+    st.step(sB, sA, pB, pA, kslot(j + 2), vslot(j), j + 1 >= n_plain, kb0 + (j + 1) * BN, issue);
   }
   if (j < nt) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, j * BN, issue);
+    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, kb0 + j * BN,
+            issue);
   }
   if (nt > 0) {
     // P V of the last tile, on a selected copy of P: two calls would leave O in different
@@ -699,64 +716,92 @@ void fa_fwd_kernel(FwdParams p) {
   compiler_fence();
 
   // ---- epilogue: O = acc / l, LSE = ln 2 * (m + log2 l) ---------------------------------------
-  // O goes through LDS so that each store instruction writes whole rows (1 KiB contiguous); stored
-  // straight from the accumulator layout, every instruction would touch 32 rows 16 bytes at a time.
-  constexpr int RB = DV * 2;           // bytes per output row
-  constexpr int WROWS = 32 * QB;       // rows per wave
-  static_assert(C::NWAVES * WROWS * RB <= C::LDS_BYTES, "output staging fits in the ring slots");
-  unsigned char* stage = smem + wave * WROWS * RB;
+  if constexpr (C::SPLIT) {
+    // Partial result of this part of the key range, for the merge pass: O normalised by this part's
+    // row sum (fp32, 16 bytes per lane and block) and this part's LSE; an empty part gives O = 0 and
+    // LSE = -inf, which the merge weighs with 0.
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int db = 0; db < A::DB; ++db) agpr_fence(st.oacc[db][qb]);
-  {
-    const int osw = o_swizzle<DV>(st.i32) << 4;             // qb * 32 leaves the low 5 row bits alone
-    const int ohalf = (st.h ^ o_half<DV>(st.i32)) << 3;
+      for (int db = 0; db < A::DB; ++db) agpr_fence(st.oacc[db][qb]);
+    const size_t head_rows = ((size_t)split * p.batch * p.hq + (size_t)b * p.hq + hq) * p.sq;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       const float l_tot = half_swap_sum(st.l_run[qb]);
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      unsigned char* srow = stage + (qb * 32 + st.i32) * RB + ohalf;
-#pragma unroll
-      for (int db = 0; db < A::DB; ++db)
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const int c = 4 * db + g4;  // 16-byte chunk: dims 8c .. 8c+7, this lane's half 4h .. 4h+3
-          const uint32_t w0 = pack_bf16x2(st.oacc[db][qb][4 * g4] * inv, st.oacc[db][qb][4 * g4 + 1] * inv);
-          const uint32_t w1 = pack_bf16x2(st.oacc[db][qb][4 * g4 + 2] * inv, st.oacc[db][qb][4 * g4 + 3] * inv);
-          *reinterpret_cast<uint2*>(srow + ((c << 4) ^ osw)) = make_uint2(w0, w1);
-        }
       const int row = st.qw + qb * 32 + st.i32;
-      if (p.lse != nullptr && st.h == 0 && row < p.sq)
-        p.lse[(size_t)(b * p.hq + hq) * p.sq + row] =
-            l_tot > 0.f ? (st.m_run[qb] + log2f(l_tot)) * kLn2 : -INFINITY;
+      if (row < p.sq) {
+        float* orow = p.o_part + (head_rows + row) * DV;
+#pragma unroll
+        for (int db = 0; db < A::DB; ++db)
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4)
+            *reinterpret_cast<f32x4*>(orow + db * 32 + 8 * g4 + 4 * st.h) =
+                f32x4{st.oacc[db][qb][4 * g4] * inv, st.oacc[db][qb][4 * g4 + 1] * inv,
+                      st.oacc[db][qb][4 * g4 + 2] * inv, st.oacc[db][qb][4 * g4 + 3] * inv};
+        if (st.h == 0) p.lse_part[head_rows + row] = l_tot > 0.f ? (st.m_run[qb] + log2f(l_tot)) * kLn2 : -INFINITY;
+      }
     }
-  }
-  // Each wave reads back only its own rows, so no barrier: LDS serves one wave's accesses in order.
-  {
-    constexpr int CPR = RB / 16;        // 16-byte chunks per row
-    constexpr int RPI = 64 / CPR;       // rows per store instruction
-    const int c = lane % CPR;
-    uint16_t* ohead = p.o + (size_t)(b * p.hq + hq) * p.sq * DV;
-    // All reads first, pinned before the stores as a group: the compiler would otherwise sink each
-    // read into its store's row guard and wait out an LDS round trip per store.
-    constexpr int NIT = WROWS / RPI;
-    u32x4 ov[NIT];
-#pragma unroll
-    for (int it = 0; it < NIT; ++it) {
-      const int r = it * RPI + lane / CPR;
-      const unsigned char* chunk = stage + r * RB + ((c ^ o_swizzle<DV>(r)) << 4);
-      const int hl = o_half<DV>(r) << 3;
-      const uint2 x = *reinterpret_cast<const uint2*>(chunk + hl);
-      const uint2 y = *reinterpret_cast<const uint2*>(chunk + (hl ^ 8));
-      ov[it] = u32x4{x.x, x.y, y.x, y.y};
+  } else {
+    // O goes through LDS so that each store instruction writes whole rows (1 KiB contiguous); stored
+    // straight from the accumulator layout, every instruction would touch 32 rows 16 bytes at a time.
+    constexpr int RB = DV * 2;           // bytes per output row
+    constexpr int WROWS = 32 * QB;       // rows per wave
+    static_assert(C::NWAVES * WROWS * RB <= C::LDS_BYTES, "output staging fits in the ring slots");
+    unsigned char* stage = smem + wave * WROWS * RB;
+  #pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+  #pragma unroll
+      for (int db = 0; db < A::DB; ++db) agpr_fence(st.oacc[db][qb]);
+    {
+      const int osw = o_swizzle<DV>(st.i32) << 4;             // qb * 32 leaves the low 5 row bits alone
+      const int ohalf = (st.h ^ o_half<DV>(st.i32)) << 3;
+  #pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const float l_tot = half_swap_sum(st.l_run[qb]);
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        unsigned char* srow = stage + (qb * 32 + st.i32) * RB + ohalf;
+  #pragma unroll
+        for (int db = 0; db < A::DB; ++db)
+  #pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int c = 4 * db + g4;  // 16-byte chunk: dims 8c .. 8c+7, this lane's half 4h .. 4h+3
+            const uint32_t w0 = pack_bf16x2(st.oacc[db][qb][4 * g4] * inv, st.oacc[db][qb][4 * g4 + 1] * inv);
+            const uint32_t w1 = pack_bf16x2(st.oacc[db][qb][4 * g4 + 2] * inv, st.oacc[db][qb][4 * g4 + 3] * inv);
+            *reinterpret_cast<uint2*>(srow + ((c << 4) ^ osw)) = make_uint2(w0, w1);
+          }
+        const int row = st.qw + qb * 32 + st.i32;
+        if (p.lse != nullptr && st.h == 0 && row < p.sq)
+          p.lse[(size_t)(b * p.hq + hq) * p.sq + row] =
+              l_tot > 0.f ? (st.m_run[qb] + log2f(l_tot)) * kLn2 : -INFINITY;
+      }
     }
-#pragma unroll
-    for (int it = 0; it < NIT; ++it) asm volatile("" : "+v"(ov[it]));
-#pragma unroll
-    for (int it = 0; it < NIT; ++it) {
-      const int row = st.qw + it * RPI + lane / CPR;
-      if (row < p.sq) *reinterpret_cast<u32x4*>(ohead + (size_t)row * DV + c * 8) = ov[it];
+    // Each wave reads back only its own rows, so no barrier: LDS serves one wave's accesses in order.
+    {
+      constexpr int CPR = RB / 16;        // 16-byte chunks per row
+      constexpr int RPI = 64 / CPR;       // rows per store instruction
+      const int c = lane % CPR;
+      uint16_t* ohead = p.o + (size_t)(b * p.hq + hq) * p.sq * DV;
+      // All reads first, pinned before the stores as a group: the compiler would otherwise sink each
+      // read into its store's row guard and wait out an LDS round trip per store.
+      constexpr int NIT = WROWS / RPI;
+      u32x4 ov[NIT];
+  #pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        const int r = it * RPI + lane / CPR;
+        const unsigned char* chunk = stage + r * RB + ((c ^ o_swizzle<DV>(r)) << 4);
+        const int hl = o_half<DV>(r) << 3;
+        const uint2 x = *reinterpret_cast<const uint2*>(chunk + hl);
+        const uint2 y = *reinterpret_cast<const uint2*>(chunk + (hl ^ 8));
+        ov[it] = u32x4{x.x, x.y, y.x, y.y};
+      }
+  #pragma unroll
+      for (int it = 0; it < NIT; ++it) asm volatile("" : "+v"(ov[it]));
+  #pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        const int row = st.qw + it * RPI + lane / CPR;
+        if (row < p.sq) *reinterpret_cast<u32x4*>(ohead + (size_t)row * DV + c * 8) = ov[it];
+      }
     }
   }
 }
@@ -774,19 +819,60 @@ void fa_fwd_kernel(FwdParams p) {
 #define FA_QB 2
 #endif
 
-template <int DQK, int DV, bool CAUSAL>
+template <int DQK, int DV, bool CAUSAL, bool SPLIT = false>
 struct Instance {
-  using C = Cfg<DQK, DV, FA_BN, FA_NWAVES, FA_QB, CAUSAL>;
+  using C = Cfg<DQK, DV, FA_BN, FA_NWAVES, FA_QB, CAUSAL, SPLIT>;
 };
 
-template <int DQK, int DV, bool CAUSAL>
+template <int DQK, int DV, bool CAUSAL, bool SPLIT>
 hipError_t launch_instance(FwdParams p, hipStream_t stream) {
-  using C = typename Instance<DQK, DV, CAUSAL>::C;
+  using C = typename Instance<DQK, DV, CAUSAL, SPLIT>::C;
   p.n_qtiles = (p.sq + C::BM - 1) / C::BM;
   p.n_wg = p.batch * p.hq * p.n_qtiles;
   void* args[] = {&p};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel<C>), dim3(p.n_wg), dim3(C::NT), args, 0,
-                         stream);
+  return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel<C>), dim3(p.n_wg * (SPLIT ? p.n_split : 1)),
+                         dim3(C::NT), args, 0, stream);
+}
+
+template <bool SPLIT>
+hipError_t launch_dims(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream) {
+  if (d_qk == 64 && d_v == 64)
+    return causal ? launch_instance<64, 64, true, SPLIT>(p, stream) : launch_instance<64, 64, false, SPLIT>(p, stream);
+  if (d_qk == 128 && d_v == 128)
+    return causal ? launch_instance<128, 128, true, SPLIT>(p, stream) : launch_instance<128, 128, false, SPLIT>(p, stream);
+  if (d_qk == 192 && d_v == 128)
+    return causal ? launch_instance<192, 128, true, SPLIT>(p, stream) : launch_instance<192, 128, false, SPLIT>(p, stream);
+  return hipErrorInvalidValue;
+}
+
+// Merge of the n_split partial results of every query row (log-sum-exp combination): with
+// M = max_s LSE_s, w_s = exp(LSE_s - M), O = sum_s w_s O_s / sum_s w_s and LSE = M + ln(sum_s w_s).
+// A row whose parts are all empty (LSE_s = -inf) gets O = 0 and LSE = -inf. One thread per row and
+// 4 output dims; reads fp32, writes bf16 (round to nearest even) and the fp32 LSE.
+template <int DV>
+__global__ __launch_bounds__(256) void fa_merge_kernel(MergeParams p) {
+  constexpr int TPR = DV / 4;  // threads per row
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = gid / TPR;
+  const int q = (int)(gid % TPR);
+  if (row >= p.rows) return;
+  float m = -INFINITY;
+  for (int sp = 0; sp < p.n_split; ++sp) m = fmaxf(m, p.lse_part[sp * p.rows + row]);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float den = 0.f;
+  if (m != -INFINITY) {
+    for (int sp = 0; sp < p.n_split; ++sp) {
+      const float w = expf(p.lse_part[sp * p.rows + row] - m);
+      den += w;
+      acc += w * *reinterpret_cast<const f32x4*>(p.o_part + (sp * p.rows + row) * DV + 4 * q);
+    }
+    acc *= 1.f / den;
+  }
+  f32x2 lo = {acc.x, acc.y}, hi = {acc.z, acc.w};
+  *reinterpret_cast<uint2*>(p.o + row * DV + 4 * q) =
+      make_uint2(bit_cast<uint32_t>(__builtin_convertvector(lo, bf16x2)),
+                 bit_cast<uint32_t>(__builtin_convertvector(hi, bf16x2)));
+  if (q == 0 && p.lse != nullptr) p.lse[row] = m == -INFINITY ? -INFINITY : m + logf(den);
 }
 
 }  // namespace
@@ -800,12 +886,25 @@ int block_rows(int d_qk, int d_v, bool causal) {
 }
 
 hipError_t launch_forward(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream) {
-  if (d_qk == 64 && d_v == 64) return causal ? launch_instance<64, 64, true>(p, stream) : launch_instance<64, 64, false>(p, stream);
-  if (d_qk == 128 && d_v == 128)
-    return causal ? launch_instance<128, 128, true>(p, stream) : launch_instance<128, 128, false>(p, stream);
-  if (d_qk == 192 && d_v == 128)
-    return causal ? launch_instance<192, 128, true>(p, stream) : launch_instance<192, 128, false>(p, stream);
-  return hipErrorInvalidValue;
+  return launch_dims<false>(p, d_qk, d_v, causal, stream);
+}
+
+hipError_t launch_forward_split(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream) {
+  const hipError_t e = launch_dims<true>(p, d_qk, d_v, causal, stream);
+  if (e != hipSuccess) return e;
+  MergeParams m;
+  m.o_part = p.o_part;
+  m.lse_part = p.lse_part;
+  m.o = p.o;
+  m.lse = p.lse;
+  m.rows = (int64_t)p.batch * p.hq * p.sq;
+  m.n_split = p.n_split;
+  const int64_t threads = m.rows * (d_v / 4);
+  const dim3 grid((unsigned)((threads + 255) / 256));
+  void* args[] = {&m};
+  const void* k = d_v == 64 ? reinterpret_cast<const void*>(&fa_merge_kernel<64>)
+                            : reinterpret_cast<const void*>(&fa_merge_kernel<128>);
+  return hipLaunchKernel(k, grid, dim3(256), args, 0, stream);
 }
 
 }  // namespace fa

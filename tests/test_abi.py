@@ -132,3 +132,56 @@ def test_python_forward_rejects_cpu_tensors(lib):
         fa.forward(q, q, q)
     with pytest.raises(ValueError):
         fa.forward(q.float(), q, q)
+
+
+# ---- split mode (fa_fwd_split): host-side checks only ----------------------------------------------
+
+WSP = P + 0x10000  # fake, 16-byte aligned workspace address
+
+
+def call_split(**kw):
+    a = dict(Q=QP, K=KP, V=VP, O=OP, LSE=LP, B=1, Hq=4, Hkv=2, Sq=100, Sk=1000, d_qk=128, d_v=128,
+             scale=0.125, causal=1, n_split=4, ws=WSP, ws_bytes=None, stream=None)
+    a.update(kw)
+    if a["ws_bytes"] is None:
+        a["ws_bytes"] = fa.fa_fwd_split_workspace_bytes(max(a["B"], 0), max(a["Hq"], 0), max(a["Sq"], 0),
+                                                        max(a["d_v"], 0), max(a["n_split"], 0))
+    return fa.fa_fwd_split(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Sk"],
+                           a["d_qk"], a["d_v"], a["scale"], a["causal"], a["n_split"], a["ws"], a["ws_bytes"],
+                           a["stream"])
+
+
+def test_split_workspace_bytes(lib):
+    assert fa.fa_fwd_split_workspace_bytes(2, 3, 5, 128, 4) == 4 * 2 * 3 * 5 * 129 * 4
+    assert fa.fa_fwd_split_workspace_bytes(1, 1, 1, 64, 1) == 65 * 4
+    for args in ((0, 3, 5, 128, 4), (2, 0, 5, 128, 4), (2, 3, 0, 128, 4), (2, 3, 5, 0, 4), (2, 3, 5, 128, 0),
+                 (-1, 3, 5, 128, 4)):
+        assert fa.fa_fwd_split_workspace_bytes(*args) == 0
+    assert fa.fa_fwd_split_workspace_bytes(2**31 - 1, 2**31 - 1, 2**31 - 1, 128, 2**31 - 1) == 2**64 - 1
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_split=0), fa.FA_ERR_BAD_SHAPE),
+    (dict(n_split=-3), fa.FA_ERR_BAD_SHAPE),
+    (dict(n_split=0, B=-1, Q=None), fa.FA_ERR_BAD_SHAPE),
+    (dict(ws=None), fa.FA_ERR_WORKSPACE),
+    (dict(ws_bytes=100), fa.FA_ERR_WORKSPACE),
+    (dict(ws=WSP + 8), fa.FA_ERR_UNSUPPORTED),
+    # the fa_fwd_ex checks come first
+    (dict(d_qk=96, d_v=96, ws=None), fa.FA_ERR_UNSUPPORTED),
+    (dict(Q=None, ws=None), fa.FA_ERR_NULL_POINTER),
+    (dict(scale=float("nan"), ws=None), fa.FA_ERR_BAD_SCALE),
+    (dict(Sq=20_000_000, ws=None), fa.FA_ERR_BAD_SHAPE),
+    (dict(B=1, Hq=4096, Hkv=4096, Sq=4096 * 64, Sk=64, d_qk=64, d_v=64, n_split=2**20), fa.FA_ERR_BAD_SHAPE),
+])
+def test_split_invalid_arguments_are_rejected_on_host(lib, kw, status):
+    assert call_split(**kw) == status
+
+
+def test_split_empty_problems_need_no_workspace(lib):
+    assert call_split(B=0, ws=None, ws_bytes=0) == fa.FA_OK
+    assert call_split(Sq=0, Q=None, O=None, ws=None, ws_bytes=0) == fa.FA_OK
+
+
+def test_split_status_string(lib):
+    assert fa.fa_status_str(6) == "FA_ERR_WORKSPACE"
