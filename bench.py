@@ -1,18 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of the fused attention forward on one MI355X.
 
-One step = one forward pass of the whole hot path (one kernel launch) over one batch of seeded
-synthetic input already resident in HBM. Prints ONE JSON line:
+One step = one forward pass of the whole hot path (one kernel launch; in split mode the part kernel
+and the merge kernel) over one batch of seeded synthetic input already resident in HBM. Prints ONE
+JSON line:
 
 * value      -- whole-job GEMM TFLOP/s: 2*B*Hq*Sq*Sk*(d_qk+d_v) (halved for causal) per step, over
                 the wall-clock time of the timed steps (bracketed by device synchronisation)
-* roofline   -- the kernel's achieved TFLOP/s from HIP events around each launch on the launch
-                stream, against the bf16 dense MFMA peak; HBM traffic from the committed rocprofv3
-                counter summary when it was taken on the current kernel source
+* roofline   -- the step's achieved rate from HIP events around each launch on the launch stream,
+                against the bf16 dense MFMA peak (TFLOP/s) or, for workloads whose operational
+                intensity at HBM is below the ridge point (decode shapes), the HBM peak (GB/s of
+                algorithmic bytes); HBM traffic from the committed rocprofv3 counter summary when it
+                was taken on the current kernel source (default workload only)
 * cpu_baseline -- the fp64 oracle timed on this host on a bounded sample of the same workload
 * parity     -- a few seeded rows per head compared with the oracle (outside the timed region)
 
-Default workload: the Llama-style GQA prefill, B1 Hq32 Hkv8 S8192 d128 causal (config 3).
+Default workload: the Llama-style GQA prefill, B1 Hq32 Hkv8 S8192 d128 causal (config 3). Split mode:
+``--split N|auto`` with ``--workload decode-128k`` (and the other named decode shapes).
 """
 
 from __future__ import annotations
@@ -29,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6  # 256 CUs x 4096 dense bf16 FLOP/clk/CU x 2.4 GHz
+PEAK_HBM_GBS = 8000.0      # HBM3E
 KERNEL_SOURCES = ["paper_2609_21264_amd/csrc/fa_fwd_kernel.hip", "paper_2609_21264_amd/csrc/fa_api.hip",
                   "paper_2609_21264_amd/csrc/fa_internal.h"]
 
@@ -132,6 +137,11 @@ def main():
                     help="untimed steps first; default: at least 10 and at least 0.5 s (the first tens of "
                          "milliseconds of back-to-back launches run slower while clocks and caches settle)")
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--workload", default=None,
+                    help="a named further workload instead of --config (split-mode shapes: "
+                         "decode-128k, decode16-128k-causal, decode-b8-8k)")
+    ap.add_argument("--split", default=None,
+                    help="run split mode (fa_fwd_split) with this many key-range parts, or 'auto'")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -149,7 +159,7 @@ def main():
     import paper_2609_21264_amd as fa
     import workloads as W
 
-    w = W.CONFIGS[args.config]
+    w = W.EXTRA[args.workload] if args.workload else W.CONFIGS[args.config]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     print(f"[bench] workload {args.config}: {w.name}", file=sys.stderr, flush=True)
@@ -160,9 +170,22 @@ def main():
     stream = torch.cuda.current_stream(dev)
     handle = stream.cuda_stream
 
+    n_split = 0
+    if args.split is not None:
+        n_split = (fa.fa_fwd_split_parts(torch.cuda.get_device_properties(dev).multi_processor_count, w.B, w.Hq,
+                                         w.Sq, w.Sk, w.dqk, w.dv, w.causal)
+                   if args.split == "auto" else int(args.split))
+        ws_bytes = fa.fa_fwd_split_workspace_bytes(w.B, w.Hq, w.Sq, w.dv, n_split)
+        ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)  # allocated before timing
+
     def step():
-        st = fa.fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), w.B, w.Hq,
-                          w.Hkv, w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, handle)
+        if n_split:
+            st = fa.fa_fwd_split(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), w.B,
+                                 w.Hq, w.Hkv, w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, n_split, ws.data_ptr(),
+                                 ws_bytes, handle)
+        else:
+            st = fa.fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), w.B, w.Hq,
+                              w.Hkv, w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, handle)
         if st != 0:
             raise fa.FaError(st)
 
@@ -206,7 +229,18 @@ def main():
     value = flops * args.steps / wall / 1e12
     avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
     achieved = flops / avg_launch_s / 1e12
-    traffic = traffic_from_profile(args.config)
+    traffic = traffic_from_profile(args.config) if not args.workload and not n_split else None
+    # Bound by operational intensity at HBM (metric FLOPs over algorithmic bytes) against the ridge
+    # point of the two peaks.
+    nbytes = W.algorithmic_bytes(w)
+    hbm_bound = flops / nbytes < PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if hbm_bound:
+        ach_gbs = nbytes / avg_launch_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach_gbs / PEAK_HBM_GBS, 4)}
+    else:
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
 
     if args.copy_calibration > 0:
         n = args.copy_calibration * (1 << 20) // 4
@@ -241,9 +275,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Sq": w.Sq, "Sk": w.Sk,
-                   "d_qk": w.dqk, "d_v": w.dv, "causal": w.causal, "scale": w.scale, "seed": w.seed},
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                   "d_qk": w.dqk, "d_v": w.dv, "causal": w.causal, "scale": w.scale, "seed": w.seed,
+                   "split": n_split or None},
+        "roofline": {**roof,
                      "traffic": traffic,
                      "kernel_ms": {"mean": round(sum(launch_ms) / len(launch_ms), 4), "min": round(min(launch_ms), 4)},
                      "algorithmic_flops_per_launch": flops,

@@ -121,6 +121,12 @@ fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, f
  * or n_split is <= 0 (nothing to store); SIZE_MAX if the count overflows. */
 size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split);
 
+/* Suggested n_split for fa_fwd_split on a device with n_cu compute units: about two workgroups per
+ * CU over all parts, no part shorter than 8 key tiles (512 keys), at least 1 (1 means the single
+ * pass fa_fwd_ex is the better call). Host arithmetic only, no HIP call. Returns 0 for unsupported
+ * head dimensions or n_cu, B, Hq, Sq <= 0 or Sk < 0. */
+int fa_fwd_split_parts(int n_cu, int B, int Hq, int Sq, int Sk, int d_qk, int d_v, int causal);
+
 /* Static, human-readable name of a status code ("FA_OK", ...); "unknown status" otherwise. */
 const char* fa_status_str(fa_status_t s);
 

@@ -20,8 +20,8 @@ from . import _lib
 from ._lib import (FA_ERR_BAD_SCALE, FA_ERR_BAD_SHAPE, FA_ERR_HIP, FA_ERR_NULL_POINTER,  # noqa: F401
                    FA_ERR_UNSUPPORTED, FA_ERR_WORKSPACE, FA_OK, LIB_PATH)
 
-__all__ = ["fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_status_str",
-           "fa_block_rows", "forward", "FaError", "LIB_PATH"]
+__all__ = ["fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
+           "fa_status_str", "fa_block_rows", "forward", "FaError", "LIB_PATH"]
 
 
 class FaError(RuntimeError):
@@ -66,14 +66,21 @@ def fa_fwd_split_workspace_bytes(B: int, Hq: int, Sq: int, d_v: int, n_split: in
     return int(_lib.load().fa_fwd_split_workspace_bytes(int(B), int(Hq), int(Sq), int(d_v), int(n_split)))
 
 
+def fa_fwd_split_parts(n_cu: int, B: int, Hq: int, Sq: int, Sk: int, d_qk: int, d_v: int, causal: bool) -> int:
+    """C ``fa_fwd_split_parts``."""
+    return int(_lib.load().fa_fwd_split_parts(int(n_cu), int(B), int(Hq), int(Sq), int(Sk), int(d_qk), int(d_v),
+                                              int(bool(causal))))
+
+
 def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return_lse: bool = False,
-            out=None, lse=None, stream=None, n_split: int = 1):
+            out=None, lse=None, stream=None, n_split=1):
     """Attention forward over contiguous bf16 BHSD torch tensors on one GPU.
 
     q [B, Hq, Sq, d_qk], k [B, Hkv, Sk, d_qk], v [B, Hkv, Sk, d_v]; returns O [B, Hq, Sq, d_v] (bf16)
     and, with ``return_lse``, LSE [B, Hq, Sq] (float32, natural log). ``scale`` defaults to
     1/sqrt(d_qk). ``n_split`` > 1 runs split mode (``fa_fwd_split``) with that many key-range parts
-    per query block and a workspace from torch's allocator. The kernels are enqueued on ``stream``
+    per query block and a workspace from torch's allocator; ``n_split="auto"`` takes the count
+    ``fa_fwd_split_parts`` suggests for the device. The kernels are enqueued on ``stream``
     (default: torch's current stream); the call does not synchronise.
     """
     import torch
@@ -108,6 +115,9 @@ def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return
         stream = torch.cuda.current_stream(q.device)
     handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
     name = "fa_fwd_ex"
+    if n_split == "auto":
+        n_cu = torch.cuda.get_device_properties(q.device).multi_processor_count
+        n_split = fa_fwd_split_parts(n_cu, B, Hq, Sq, Sk, dqk, dv, causal)
     with torch.cuda.device(q.device):
         if n_split is not None and int(n_split) > 1:
             name = "fa_fwd_split"

@@ -22,8 +22,8 @@ FA_ERR_HIP = 5
 FA_ERR_WORKSPACE = 6
 
 #: Symbols include/fa.h declares.
-EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_status_str",
-            "fa_block_rows")
+EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
+            "fa_status_str", "fa_block_rows")
 
 _lib = None
 
@@ -48,6 +48,8 @@ def load() -> ctypes.CDLL:
     lib.fa_fwd_split.restype = i
     lib.fa_fwd_split_workspace_bytes.argtypes = [i, i, i, i, i]
     lib.fa_fwd_split_workspace_bytes.restype = ctypes.c_size_t
+    lib.fa_fwd_split_parts.argtypes = [i, i, i, i, i, i, i, i]
+    lib.fa_fwd_split_parts.restype = i
     lib.fa_status_str.argtypes = [i]
     lib.fa_status_str.restype = ctypes.c_char_p
     lib.fa_block_rows.argtypes = [i, i, i]

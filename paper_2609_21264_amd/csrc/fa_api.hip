@@ -105,6 +105,18 @@ fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, f
                  workspace_bytes);
 }
 
+int fa_fwd_split_parts(int n_cu, int B, int Hq, int Sq, int Sk, int d_qk, int d_v, int causal) {
+  const int bm = fa::block_rows(d_qk, d_v, causal != 0);
+  if (bm == 0 || n_cu <= 0 || B <= 0 || Hq <= 0 || Sq <= 0 || Sk < 0) return 0;
+  // Enough workgroups for about two per CU, but no part shorter than 8 key tiles (the fixed cost of
+  // a workgroup and of the merge would dominate). The query block with the most keys sees all Sk.
+  const int64_t items = static_cast<int64_t>(B) * Hq * ((static_cast<int64_t>(Sq) + bm - 1) / bm);
+  const int64_t max_parts = (static_cast<int64_t>(Sk) + 64 * 8 - 1) / (64 * 8);
+  int64_t parts = (2 * static_cast<int64_t>(n_cu)) / items;
+  if (parts > max_parts) parts = max_parts;
+  return parts < 1 ? 1 : static_cast<int>(parts);
+}
+
 size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split) {
   const int64_t n = split_workspace_bytes(B, Hq, Sq, d_v, n_split);
   return n < 0 ? SIZE_MAX : static_cast<size_t>(n);

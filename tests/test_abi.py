@@ -185,3 +185,19 @@ def test_split_empty_problems_need_no_workspace(lib):
 
 def test_split_status_string(lib):
     assert fa.fa_status_str(6) == "FA_ERR_WORKSPACE"
+
+
+def test_split_parts_heuristic(lib):
+    # decode: 32 query blocks on 256 CUs, 2048 key tiles -> 16 parts (two workgroups per CU)
+    assert fa.fa_fwd_split_parts(256, 1, 32, 1, 131072, 128, 128, 0) == 16
+    # many query blocks: no split
+    assert fa.fa_fwd_split_parts(256, 1, 32, 8192, 8192, 128, 128, 1) == 1
+    # 256 blocks: two parts
+    assert fa.fa_fwd_split_parts(256, 8, 32, 1, 8192, 128, 128, 0) == 2
+    # short keys cap the parts at 8 tiles each
+    assert fa.fa_fwd_split_parts(256, 1, 1, 256, 256, 64, 64, 0) == 1
+    assert fa.fa_fwd_split_parts(256, 1, 1, 256, 2048, 64, 64, 0) == 4
+    # invalid
+    assert fa.fa_fwd_split_parts(256, 1, 1, 1, 64, 96, 96, 0) == 0
+    assert fa.fa_fwd_split_parts(0, 1, 1, 1, 64, 64, 64, 0) == 0
+    assert fa.fa_fwd_split_parts(256, 1, 0, 1, 64, 64, 64, 0) == 0

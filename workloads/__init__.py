@@ -66,6 +66,18 @@ CONFIGS: Dict[int, Workload] = {
 }
 
 
+#: Further workloads for split mode (few query rows against long keys), by name.
+EXTRA: Dict[str, Workload] = {
+    "decode-128k": Workload(name="decode B1 Hq32 Hkv8 Sq1 Sk131072 d128", B=1, Hq=32, Hkv=8, Sq=1, Sk=131072,
+                            dqk=128, dv=128, causal=False, scale=1.0 / math.sqrt(128), seed=1101),
+    "decode16-128k-causal": Workload(name="decode B1 Hq32 Hkv8 Sq16 Sk131072 d128 causal", B=1, Hq=32, Hkv=8,
+                                     Sq=16, Sk=131072, dqk=128, dv=128, causal=True,
+                                     scale=1.0 / math.sqrt(128), seed=1102),
+    "decode-b8-8k": Workload(name="decode B8 Hq32 Hkv8 Sq1 Sk8192 d128", B=8, Hq=32, Hkv=8, Sq=1, Sk=8192,
+                             dqk=128, dv=128, causal=False, scale=1.0 / math.sqrt(128), seed=1103),
+}
+
+
 def make_inputs(w: Workload, device: str = "cpu") -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """Draw Q, K, V (bf16, contiguous BHSD) for workload ``w`` from its seed.
 
