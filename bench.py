@@ -128,6 +128,60 @@ def parity_sample(w, q, k, v, o, lse, rows_per_head: int = 4):
             "pass": bool(max_abs <= 2e-2 and lse_max <= 1e-3)}
 
 
+def paper_sweep():
+    """Steady-state timing of the paper's shapes; one JSON line. For each shape: 0.3 s of warmup
+    launches, then at least 20 launches and 0.2 s timed with events on the launch stream."""
+    import torch
+
+    import paper_2609_21264_amd as fa
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    rows = []
+    for source, w, paper_us in W.PAPER_SWEEP:
+        q, k, v = (x.to(dev) for x in W.make_inputs(w))
+        o = torch.empty((w.B, w.Hq, w.Sq, w.dv), dtype=torch.bfloat16, device=dev)
+        lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+
+        def step():
+            st = fa.fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), w.B, w.Hq,
+                              w.Hkv, w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, stream.cuda_stream)
+            if st != 0:
+                raise fa.FaError(st)
+
+        torch.cuda.synchronize()
+        t_w, n_w = time.perf_counter(), 0
+        while n_w < 10 or time.perf_counter() - t_w < 0.3:
+            step()
+            n_w += 1
+            torch.cuda.synchronize()
+        per = (time.perf_counter() - t_w) / n_w
+        n = max(20, int(0.2 / per) + 1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / n
+        ns_flops = W.metric_flops(w)
+        paper_flops = W.paper_flops(w.Hq, w.Sq, w.Sk, w.dqk, w.dv, w.B)
+        rows.append({"source": source, "shape": w.name, "H": w.Hq, "Hkv": w.Hkv, "S": w.Sq, "d": w.dqk,
+                     "causal": w.causal, "ms": round(ms, 4),
+                     "tflops_metric": round(ns_flops / (ms * 1e-3) / 1e12, 2),
+                     "tflops_paper_convention": round(paper_flops / (ms * 1e-3) / 1e12, 2),
+                     "paper_xdna2_ms": paper_us / 1e3, "speedup_vs_paper_xdna2": round(paper_us / 1e3 / ms, 1)})
+        print(f"[sweep] {w.name}: {ms:.4f} ms, {rows[-1]['tflops_metric']} TFLOP/s", file=sys.stderr, flush=True)
+        del q, k, v, o, lse
+    print(json.dumps({"metric": "attention fwd on the paper's shapes, 1 MI355X", "unit": "ms / TFLOP/s",
+                      "data": "synthetic", "dtype": "bf16", "n_gpus": 1,
+                      "note": "tflops_metric halves causal FLOPs; tflops_paper_convention does not (the paper's "
+                              "P_effGEMM); paper_xdna2_ms is the paper's measured latency on its NPU (context)",
+                      "rows": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +194,9 @@ def main():
     ap.add_argument("--workload", default=None,
                     help="a named further workload instead of --config (split-mode shapes: "
                          "decode-128k, decode16-128k-causal, decode-b8-8k)")
+    ap.add_argument("--paper-sweep", action="store_true",
+                    help="time the paper's own shapes (Table 5 GPT-2 Small sweep and the 12 Table 6 models) "
+                         "and print one JSON line with a row per shape, in both FLOP conventions")
     ap.add_argument("--split", default=None,
                     help="run split mode (fa_fwd_split) with this many key-range parts, or 'auto'")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
@@ -149,6 +206,9 @@ def main():
                          "kernel of known traffic for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
+    if args.paper_sweep:
+        paper_sweep()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the fused attention kernel runs on a "
               "single MI355X and this build has no multi-GPU path.", file=sys.stderr)

@@ -78,6 +78,33 @@ EXTRA: Dict[str, Workload] = {
 }
 
 
+def _paper(name: str, H: int, Hkv: int, S: int, d: int, causal: bool, seed: int) -> Workload:
+    return Workload(name=name, B=1, Hq=H, Hkv=Hkv, Sq=S, Sk=S, dqk=d, dv=d, causal=causal,
+                    scale=1.0 / math.sqrt(d), seed=seed)
+
+
+#: The paper's own shapes with its XDNA 2 latencies in microseconds, as context for a like-for-like
+#: comparison (the paper's hardware, not a target): the GPT-2 Small attention sweep of Table 5 (H=12,
+#: d=64, causal, B=1, Sec. 6.1) and the twelve model configurations of Table 6 (Sec. 6.5).
+PAPER_SWEEP: List[Tuple[str, Workload, float]] = [
+    *[("Table 5", _paper(f"GPT-2 Small attention S{S}", 12, 12, S, 64, True, 1200 + i), us)
+      for i, (S, us) in enumerate([(256, 300.0), (512, 600.0), (1024, 1700.0), (2048, 5200.0), (4096, 17200.0),
+                                   (8192, 62000.0), (16384, 234500.0), (32768, 911100.0)])],
+    ("Table 6", _paper("BERT-Base S2048", 12, 12, 2048, 64, False, 1300), 5775.0),
+    ("Table 6", _paper("BERT-Large S2048", 16, 16, 2048, 64, False, 1301), 7526.0),
+    ("Table 6", _paper("GPT-2 Small / OPT-125M S2048", 12, 12, 2048, 64, True, 1302), 5810.0),
+    ("Table 6", _paper("GPT-2 Medium S2048", 16, 16, 2048, 64, True, 1303), 7535.0),
+    ("Table 6", _paper("GPT-2 Large S2048", 20, 20, 2048, 64, True, 1304), 9196.0),
+    ("Table 6", _paper("Llama-2 7B S2048", 32, 32, 2048, 128, True, 1305), 34201.0),
+    ("Table 6", _paper("Llama-3 8B S2048", 32, 8, 2048, 128, True, 1306), 34076.0),
+    ("Table 6", _paper("Qwen1.5-0.5B S32768", 16, 16, 32768, 64, True, 1307), 1214700.0),
+    ("Table 6", _paper("Qwen2.5-0.5B-Instruct S32768", 14, 2, 32768, 64, True, 1308), 1062870.0),
+    ("Table 6", _paper("Qwen1.5-0.5B S131072", 16, 16, 131072, 64, True, 1309), 18996700.0),
+    ("Table 6", _paper("DeepSeek LLM 7B S4096", 32, 32, 4096, 128, True, 1310), 114443.0),
+    ("Table 6", _paper("DeepSeek LLM 67B S4096", 64, 8, 4096, 128, True, 1311), 227467.0),
+]
+
+
 def make_inputs(w: Workload, device: str = "cpu") -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """Draw Q, K, V (bf16, contiguous BHSD) for workload ``w`` from its seed.
 
