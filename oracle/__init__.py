@@ -11,6 +11,9 @@ Contents (all NumPy float64 or plain Python, no GPU):
   algorithm (Alg. 1) and the tile-to-tile split/merge (Alg. 2, with the merge read as the standard
   log-sum-exp combination). Used to cross-check the naive oracle.
 * :mod:`oracle.brute` -- scalar double loops over Python floats with ``math.exp``, for tiny inputs.
+* :mod:`oracle.layer_by_layer` -- the paper's unfused layer-by-layer mapping as three operators with
+  bfloat16 intermediates (score matrix, probabilities), the oracle of the unfused GPU baseline, with
+  a direct float64 -> bfloat16 rounding and the error bound of the three roundings.
 * :func:`bf16_bits_to_f64` -- exact decoding of bfloat16 bit patterns.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against facts that do not come from the
@@ -20,3 +23,5 @@ oracle itself: torch's float64 CPU attention routine, closed forms, invariances,
 from .naive import attention_head, bf16_bits_to_f64, naive_attention, naive_attention_rows  # noqa: F401
 from .tiled import flash_tile, spatial_flash_attention  # noqa: F401
 from .brute import brute_attention  # noqa: F401
+from .layer_by_layer import (lbl_error_bound, lbl_pv_head, lbl_scores_head, lbl_softmax_head,  # noqa: F401
+                             layer_by_layer_attention, round_bf16)
