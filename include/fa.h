@@ -1,5 +1,6 @@
 /*
- * fa.h -- C ABI of the fused attention forward for AMD Instinct MI355X (gfx950).
+ * fa.h -- C ABI of the attention forward for AMD Instinct MI355X (gfx950): the fused kernel, its
+ * split mode, and the unfused layer-by-layer operators it is measured against.
  *
  * Operation (the paper's scaled dot-product attention, Eq. (1), Sec. 2.1, replicated over heads):
  *
@@ -126,6 +127,76 @@ size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split)
  * pass fa_fwd_ex is the better call). Host arithmetic only, no HIP call. Returns 0 for unsupported
  * head dimensions or n_cu, B, Hq, Sq <= 0 or Sk < 0. */
 int fa_fwd_split_parts(int n_cu, int B, int Hq, int Sq, int Sk, int d_qk, int d_v, int causal);
+
+/*
+ * Layer-by-layer (unfused) attention -- the paper's diagnostic baseline mapping (Sec. "Diagnostic
+ * Baseline: Unfused Layer-by-Layer Attention"): the same operation as three operators dispatched
+ * one after another, each reading its input from device memory and writing its result back, with
+ * the intermediates in bfloat16 (Table 3 lists the score matrix QK^T and the probability matrix
+ * among what this mapping spills):
+ *
+ *   fa_lbl_scores:   S[b,h,i,j] = bf16(scale * q_i . k_j)                (fp32 accumulation, RNE)
+ *   fa_lbl_softmax:  LSE[b,h,i] = ln sum over visible j of exp(S[b,h,i,j]);
+ *                    P[b,h,i,j] = bf16(exp(S[b,h,i,j] - LSE[b,h,i])) for visible j, 0 for masked j
+ *   fa_lbl_pv:       O[b,h,i,:] = bf16(sum over j of P[b,h,i,j] * V[b,g,j,:])  (fp32 accumulation)
+ *
+ * It exists to measure what fusion saves; fa_fwd_ex is the operation's fast path. Results differ
+ * from fa_fwd_ex by the roundings of S and P: per output row at most
+ * max|V| * ((1 + u)^2 * exp(2 u M) - 1) with u = 2^-8 and M the row's largest visible |score|, plus
+ * fp32 accumulation error.
+ *
+ * Spill buffers S and P: bf16 [B][Hq][Sq][ld] with row stride ld = fa_lbl_ld(Sk) (Sk rounded up to
+ * 64), 16-byte aligned, owned by the caller. Row extents: query rows are taken in blocks of 128
+ * (rows 128*c .. 128*c+127 of a head); let n be the number of keys visible to the last row of the
+ * block (Sk without causal masking); the block's extent is E = 64 * ceil(n / 64) <= ld.
+ *   - fa_lbl_scores writes S[i][j] for j < E (unmasked values, also past the diagonal) and nothing
+ *     else of S;
+ *   - fa_lbl_softmax reads S[i][j] for visible j (j < ld otherwise unread), writes P[i][j] for every
+ *     j < E (0 for masked j) and nothing else of P; P may be the same buffer as S (in place) or
+ *     disjoint from it, but must not partly overlap it;
+ *   - fa_lbl_pv reads P[i][j] and V rows j for j < E only (V rows j >= Sk count as zeros).
+ * Causal masking and GQA as for fa_fwd_ex. Supported dimensions: d_qk in {64, 128, 192} for the
+ * scores, d_v in {64, 128} for P V; Sk <= 2^22.
+ *
+ * Errors (host checks, in this order; on error nothing is launched): sizes as for fa_fwd_ex or
+ * Sk > 2^22 (FA_ERR_BAD_SHAPE), head dimension not supported (FA_ERR_UNSUPPORTED), a NULL buffer
+ * that has elements (FA_ERR_NULL_POINTER; LSE may be NULL), scale not finite (FA_ERR_BAD_SCALE), a
+ * pointer not 16-byte aligned or LSE not 4-byte aligned (FA_ERR_UNSUPPORTED). B*Hq*Sq == 0 returns
+ * FA_OK without a launch. Each operator enqueues one kernel on `stream`.
+ */
+fa_status_t fa_lbl_scores(const void* Q, const void* K, void* S, int B, int Hq, int Hkv, int Sq, int Sk,
+                          int d_qk, float scale, int causal, void* stream);
+fa_status_t fa_lbl_softmax(const void* S, void* P, float* LSE, int B, int Hq, int Sq, int Sk, int causal,
+                           void* stream);
+fa_status_t fa_lbl_pv(const void* P, const void* V, void* O, int B, int Hq, int Hkv, int Sq, int Sk, int d_v,
+                      int causal, void* stream);
+
+/* Row stride ld (elements) of the spill buffers: Sk rounded up to 64; -1 if Sk < 0 or Sk > 2^22. */
+int fa_lbl_ld(int Sk);
+
+/* Bytes of spill buffer for the whole problem, B * Hq * Sq * ld * 2; 0 if B, Hq, Sq or Sk <= 0;
+ * SIZE_MAX if Sk > 2^22 or the count overflows. */
+size_t fa_lbl_workspace_bytes(int B, int Hq, int Sq, int Sk);
+
+/*
+ * fa_fwd_unfused -- the three layer-by-layer operators in sequence on `stream`, producing O and
+ * (optionally) LSE like fa_fwd_ex. The score matrix and then, in place, the probabilities of a
+ * chunk of the problem live in `workspace` (caller-owned device memory, 16-byte aligned,
+ * overwritten; not to be touched until the work on `stream` has completed). A chunk is as many whole
+ * query heads as fit (a multiple of Hq / Hkv heads when more than that many fit) or, when one head
+ * does not fit, as many blocks of 128 query rows of one head as fit; each chunk is three launches.
+ * workspace_bytes >= fa_lbl_workspace_bytes(B, Hq, Sq, Sk) runs the whole problem as one chunk;
+ * the least accepted is min(Sq, 128) * fa_lbl_ld(Sk) * 2. Supported dimensions: d_qk in
+ * {64, 128, 192}, d_v in {64, 128}.
+ *
+ * Errors: as for the operators (sizes, head dimensions, pointers, scale, alignment of Q, K, V, O,
+ * LSE), then workspace NULL or smaller than the least size (FA_ERR_WORKSPACE), then workspace not
+ * 16-byte aligned (FA_ERR_UNSUPPORTED). B*Hq*Sq == 0 returns FA_OK without touching the workspace.
+ * With Sk == 0 no workspace is needed and every row gets O = 0, LSE = -inf.
+ */
+fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq,
+                           int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
+                           void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static, human-readable name of a status code ("FA_OK", ...); "unknown status" otherwise. */
 const char* fa_status_str(fa_status_t s);

@@ -1,4 +1,4 @@
-"""Fused attention forward for AMD Instinct MI355X (gfx950).
+"""Attention forward for AMD Instinct MI355X (gfx950): the fused kernel and the unfused baseline.
 
 A thin Python binding over ``libfa.so``, whose C ABI is declared in ``include/fa.h``. PyTorch only
 supplies device memory and the stream; every step of the computation runs in the library's HIP
@@ -7,8 +7,12 @@ kernel. The functions below marshal arguments and translate status codes, nothin
 * :func:`fa_fwd`, :func:`fa_fwd_ex`, :func:`fa_fwd_split`, :func:`fa_fwd_split_workspace_bytes`,
   :func:`fa_status_str`, :func:`fa_block_rows` -- the C entry points under the same names, taking raw
   device pointers (ints) and sizes.
+* :func:`fa_lbl_scores`, :func:`fa_lbl_softmax`, :func:`fa_lbl_pv`, :func:`fa_lbl_ld`,
+  :func:`fa_lbl_workspace_bytes`, :func:`fa_fwd_unfused` -- the layer-by-layer (unfused) operators
+  and their composition, under the same names.
 * :func:`forward` -- convenience wrapper over torch tensors (``n_split`` > 1 selects split mode and
   takes the workspace from torch's allocator).
+* :func:`forward_unfused` -- the same over the unfused path (``fa_fwd_unfused``).
 """
 
 from __future__ import annotations
@@ -21,7 +25,8 @@ from ._lib import (FA_ERR_BAD_SCALE, FA_ERR_BAD_SHAPE, FA_ERR_HIP, FA_ERR_NULL_P
                    FA_ERR_UNSUPPORTED, FA_ERR_WORKSPACE, FA_OK, LIB_PATH)
 
 __all__ = ["fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
-           "fa_status_str", "fa_block_rows", "forward", "FaError", "LIB_PATH"]
+           "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
+           "fa_lbl_workspace_bytes", "fa_fwd_unfused", "forward", "forward_unfused", "FaError", "LIB_PATH"]
 
 
 class FaError(RuntimeError):
@@ -70,6 +75,95 @@ def fa_fwd_split_parts(n_cu: int, B: int, Hq: int, Sq: int, Sk: int, d_qk: int, 
     """C ``fa_fwd_split_parts``."""
     return int(_lib.load().fa_fwd_split_parts(int(n_cu), int(B), int(Hq), int(Sq), int(Sk), int(d_qk), int(d_v),
                                               int(bool(causal))))
+
+
+def fa_lbl_scores(Q: int, K: int, S: int, B: int, Hq: int, Hkv: int, Sq: int, Sk: int, d_qk: int, scale: float,
+                  causal: bool, stream: int) -> int:
+    """C ``fa_lbl_scores``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_lbl_scores(Q, K, S, B, Hq, Hkv, Sq, Sk, d_qk, float(scale), int(bool(causal)), stream))
+
+
+def fa_lbl_softmax(S: int, P: int, LSE: Optional[int], B: int, Hq: int, Sq: int, Sk: int, causal: bool,
+                   stream: int) -> int:
+    """C ``fa_lbl_softmax``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_lbl_softmax(S, P, LSE, B, Hq, Sq, Sk, int(bool(causal)), stream))
+
+
+def fa_lbl_pv(P: int, V: int, O: int, B: int, Hq: int, Hkv: int, Sq: int, Sk: int, d_v: int, causal: bool,
+              stream: int) -> int:
+    """C ``fa_lbl_pv``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_lbl_pv(P, V, O, B, Hq, Hkv, Sq, Sk, d_v, int(bool(causal)), stream))
+
+
+def fa_lbl_ld(Sk: int) -> int:
+    """C ``fa_lbl_ld``: row stride (elements) of the layer-by-layer spill buffers."""
+    return int(_lib.load().fa_lbl_ld(int(Sk)))
+
+
+def fa_lbl_workspace_bytes(B: int, Hq: int, Sq: int, Sk: int) -> int:
+    """C ``fa_lbl_workspace_bytes``."""
+    return int(_lib.load().fa_lbl_workspace_bytes(int(B), int(Hq), int(Sq), int(Sk)))
+
+
+def fa_fwd_unfused(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, Hq: int, Hkv: int, Sq: int,
+                   Sk: int, d_qk: int, d_v: int, scale: float, causal: bool, workspace: Optional[int],
+                   workspace_bytes: int, stream: int) -> int:
+    """C ``fa_fwd_unfused``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_fwd_unfused(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, float(scale),
+                                          int(bool(causal)), workspace, int(workspace_bytes), stream))
+
+
+def _check_qkv(q, k, v):
+    import torch
+
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not isinstance(t, torch.Tensor) or t.dim() != 4:
+            raise ValueError(f"{name} must be a 4-d torch tensor (BHSD)")
+        if t.dtype != torch.bfloat16:
+            raise ValueError(f"{name} must be bfloat16")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on a GPU")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if not (q.device == k.device == v.device):
+        raise ValueError("q, k, v must be on the same device")
+    B, Hq, Sq, dqk = q.shape
+    Bk, Hkv, Sk, dk = k.shape
+    if Bk != B or dk != dqk or v.shape[:3] != k.shape[:3]:
+        raise ValueError(f"inconsistent shapes q{tuple(q.shape)} k{tuple(k.shape)} v{tuple(v.shape)}")
+    return B, Hq, Hkv, Sq, Sk, dqk, v.shape[3]
+
+
+def forward_unfused(q, k, v, causal: bool = False, scale: Optional[float] = None, return_lse: bool = False,
+                    workspace=None, stream=None):
+    """Attention forward through the unfused layer-by-layer path (``fa_fwd_unfused``): scores, mask +
+    softmax and P V as three kernels with S and P spilled to device memory in bf16. Same tensors and
+    defaults as :func:`forward`. ``workspace`` is a uint8 CUDA tensor for the spill buffer (default: one
+    sized for the whole problem from torch's allocator; a smaller one runs the problem in chunks)."""
+    import torch
+
+    B, Hq, Hkv, Sq, Sk, dqk, dv = _check_qkv(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(dqk)
+    out = torch.empty((B, Hq, Sq, dv), dtype=torch.bfloat16, device=q.device)
+    lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if return_lse else None
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    with torch.cuda.device(q.device):
+        if workspace is None:
+            nbytes = fa_lbl_workspace_bytes(B, Hq, Sq, Sk)
+            workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
+            if isinstance(stream, torch.cuda.Stream):
+                workspace.record_stream(stream)
+        st = fa_fwd_unfused(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                            lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, dqk, dv, scale, causal,
+                            workspace.data_ptr(), workspace.numel() * workspace.element_size(), handle)
+    if st != FA_OK:
+        if st in (FA_ERR_NULL_POINTER, FA_ERR_BAD_SHAPE, FA_ERR_UNSUPPORTED, FA_ERR_BAD_SCALE, FA_ERR_WORKSPACE):
+            raise ValueError(f"fa_fwd_unfused rejected the arguments: {fa_status_str(st)}")
+        raise FaError(st)
+    return (out, lse) if return_lse else out
 
 
 def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return_lse: bool = False,

@@ -23,7 +23,8 @@ FA_ERR_WORKSPACE = 6
 
 #: Symbols include/fa.h declares.
 EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
-            "fa_status_str", "fa_block_rows")
+            "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
+            "fa_lbl_workspace_bytes", "fa_fwd_unfused")
 
 _lib = None
 
@@ -54,5 +55,17 @@ def load() -> ctypes.CDLL:
     lib.fa_status_str.restype = ctypes.c_char_p
     lib.fa_block_rows.argtypes = [i, i, i]
     lib.fa_block_rows.restype = i
+    lib.fa_lbl_scores.argtypes = [vp, vp, vp, i, i, i, i, i, i, f, i, vp]
+    lib.fa_lbl_scores.restype = i
+    lib.fa_lbl_softmax.argtypes = [vp, vp, vp, i, i, i, i, i, vp]
+    lib.fa_lbl_softmax.restype = i
+    lib.fa_lbl_pv.argtypes = [vp, vp, vp, i, i, i, i, i, i, i, vp]
+    lib.fa_lbl_pv.restype = i
+    lib.fa_lbl_ld.argtypes = [i]
+    lib.fa_lbl_ld.restype = i
+    lib.fa_lbl_workspace_bytes.argtypes = [i, i, i, i]
+    lib.fa_lbl_workspace_bytes.restype = ctypes.c_size_t
+    lib.fa_fwd_unfused.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, vp, ctypes.c_size_t, vp]
+    lib.fa_fwd_unfused.restype = i
     _lib = lib
     return lib

@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libfa.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-SOURCES = ["fa_api.hip", "fa_fwd_kernel.hip"]
+SOURCES = ["fa_api.hip", "fa_fwd_kernel.hip", "fa_lbl_kernel.hip"]
 ARCH = "gfx950"
 
 
@@ -56,11 +56,11 @@ def compile_command(out: str, extra=()) -> list:
     ]
 
 
-def kernel_asm(out: str) -> None:
-    """Write the gfx950 assembly of the kernel translation unit to `out` (for static checks of the
-    generated code; nothing is linked)."""
+def kernel_asm(out: str, source: str = "fa_fwd_kernel.hip") -> None:
+    """Write the gfx950 assembly of one kernel translation unit (default: the fused kernel) to `out`,
+    for static checks of the generated code; nothing is linked."""
     cmd = [hipcc(), *_device_flags(), "--cuda-device-only", "-S", "-w", "-o", out,
-           os.path.join(CSRC, "fa_fwd_kernel.hip")]
+           os.path.join(CSRC, source)]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc -S failed:\n" + (res.stdout or "") + (res.stderr or ""))

@@ -1,5 +1,6 @@
-// C ABI of the fused attention forward (declared in include/fa.h): host-side argument checks, then
-// one kernel launch on the caller's stream. No allocation, no synchronisation, no global state.
+// C ABI of the attention forward (declared in include/fa.h): host-side argument checks, then kernel
+// launches on the caller's stream (fused forward, split mode, layer-by-layer operators). No
+// allocation, no synchronisation, no global state.
 #include <float.h>
 #include <limits.h>
 #include <math.h>
@@ -83,6 +84,49 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
   return err == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
 
+
+// ---- layer-by-layer operators ------------------------------------------------------------------
+
+int64_t lbl_ld(int Sk) { return (static_cast<int64_t>(Sk) + fa::kLblKeys - 1) / fa::kLblKeys * fa::kLblKeys; }
+
+// Shared checks of the layer-by-layer entry points, in the order documented in fa.h. d_qk / d_v are
+// checked only where the operator uses them (0 = unused).
+fa_status_t lbl_check_shape(int B, int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v) {
+  if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0) return FA_ERR_BAD_SHAPE;
+  if (Hq > 0 && (Hkv <= 0 || Hq % Hkv != 0)) return FA_ERR_BAD_SHAPE;
+  if (Sk > fa::kLblMaxSk) return FA_ERR_BAD_SHAPE;
+  const int64_t dmax = d_qk > d_v ? d_qk : d_v;
+  if (static_cast<int64_t>(Sq) * dmax > INT_MAX || static_cast<int64_t>(Sk) * dmax > INT_MAX) return FA_ERR_BAD_SHAPE;
+  const int64_t n_qb = (static_cast<int64_t>(Sq) + fa::kLblRows - 1) / fa::kLblRows;
+  if (static_cast<int64_t>(B) * Hq * n_qb > INT_MAX) return FA_ERR_BAD_SHAPE;
+  if (static_cast<int64_t>(B) * Hq * Sq > 4 * static_cast<int64_t>(INT_MAX)) return FA_ERR_BAD_SHAPE;
+  if (static_cast<int64_t>(B) * Hkv > INT_MAX) return FA_ERR_BAD_SHAPE;
+  if (d_qk != 0 && !fa::lbl_scores_supported(d_qk)) return FA_ERR_UNSUPPORTED;
+  if (d_v != 0 && !fa::lbl_pv_supported(d_v)) return FA_ERR_UNSUPPORTED;
+  return FA_OK;
+}
+
+// The whole problem as one chunk; spill buffers S and P.
+fa::LblParams lbl_params(int B, int Hq, int Hkv, int Sq, int Sk, float scale, int causal) {
+  fa::LblParams p{};
+  p.batch = B;
+  p.hq = Hq;
+  p.hkv = Hkv;
+  p.sq = Sq;
+  p.sk = Sk;
+  p.group = Hkv > 0 ? Hq / Hkv : 1;
+  p.causal = causal != 0;
+  p.ld = static_cast<int>(lbl_ld(Sk));
+  p.scale = scale;
+  p.bh0 = 0;
+  p.nbh = B * Hq;
+  p.qb0 = 0;
+  p.nqb = (Sq + fa::kLblRows - 1) / fa::kLblRows;
+  p.xgroup = p.group;
+  p.rows = static_cast<int64_t>(B) * Hq * Sq;
+  return p;
+}
+
 }  // namespace
 
 extern "C" {
@@ -120,6 +164,130 @@ int fa_fwd_split_parts(int n_cu, int B, int Hq, int Sq, int Sk, int d_qk, int d_
 size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split) {
   const int64_t n = split_workspace_bytes(B, Hq, Sq, d_v, n_split);
   return n < 0 ? SIZE_MAX : static_cast<size_t>(n);
+}
+
+int fa_lbl_ld(int Sk) { return Sk < 0 || Sk > fa::kLblMaxSk ? -1 : static_cast<int>(lbl_ld(Sk)); }
+
+size_t fa_lbl_workspace_bytes(int B, int Hq, int Sq, int Sk) {
+  if (B <= 0 || Hq <= 0 || Sq <= 0 || Sk <= 0) return 0;
+  if (Sk > fa::kLblMaxSk) return SIZE_MAX;
+  const int64_t bh = static_cast<int64_t>(B) * Hq;
+  const int64_t per_row = lbl_ld(Sk) * 2;  // < 2^24
+  if (bh > INT64_MAX / Sq) return SIZE_MAX;
+  const int64_t rows = bh * Sq;
+  if (rows > INT64_MAX / per_row) return SIZE_MAX;
+  return static_cast<size_t>(rows * per_row);
+}
+
+fa_status_t fa_lbl_scores(const void* Q, const void* K, void* S, int B, int Hq, int Hkv, int Sq, int Sk, int d_qk,
+                          float scale, int causal, void* stream) {
+  fa_status_t st = lbl_check_shape(B, Hq, Hkv, Sq, Sk, d_qk, 0);
+  if (st != FA_OK) return st;
+  const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
+  const bool kv_rows = static_cast<int64_t>(B) * Hkv * Sk > 0;
+  if ((q_rows && Q == nullptr) || (kv_rows && K == nullptr) || (q_rows && Sk > 0 && S == nullptr))
+    return FA_ERR_NULL_POINTER;
+  if (!isfinite(scale)) return FA_ERR_BAD_SCALE;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(S, 16)) return FA_ERR_UNSUPPORTED;
+  if (!q_rows || Sk == 0) return FA_OK;  // no score to write
+  fa::LblParams p = lbl_params(B, Hq, Hkv, Sq, Sk, scale, causal);
+  p.q = static_cast<const uint16_t*>(Q);
+  p.k = static_cast<const uint16_t*>(K);
+  p.s = static_cast<uint16_t*>(S);
+  return fa::launch_lbl_scores(p, d_qk, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+}
+
+fa_status_t fa_lbl_softmax(const void* S, void* P, float* LSE, int B, int Hq, int Sq, int Sk, int causal,
+                           void* stream) {
+  fa_status_t st = lbl_check_shape(B, Hq, Hq > 0 ? 1 : 0, Sq, Sk, 0, 0);
+  if (st != FA_OK) return st;
+  const bool rows = static_cast<int64_t>(B) * Hq * Sq > 0;
+  if (rows && Sk > 0 && (S == nullptr || P == nullptr)) return FA_ERR_NULL_POINTER;
+  if (!aligned(S, 16) || !aligned(P, 16) || !aligned(LSE, 4)) return FA_ERR_UNSUPPORTED;
+  if (!rows) return FA_OK;
+  fa::LblParams p = lbl_params(B, Hq, 1, Sq, Sk, 1.f, causal);
+  p.s = const_cast<uint16_t*>(static_cast<const uint16_t*>(S));
+  p.p = static_cast<uint16_t*>(P);
+  p.lse = LSE;
+  return fa::launch_lbl_softmax(p, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+}
+
+fa_status_t fa_lbl_pv(const void* P, const void* V, void* O, int B, int Hq, int Hkv, int Sq, int Sk, int d_v,
+                      int causal, void* stream) {
+  fa_status_t st = lbl_check_shape(B, Hq, Hkv, Sq, Sk, 0, d_v);
+  if (st != FA_OK) return st;
+  const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
+  const bool kv_rows = static_cast<int64_t>(B) * Hkv * Sk > 0;
+  if ((q_rows && O == nullptr) || (kv_rows && V == nullptr) || (q_rows && Sk > 0 && P == nullptr))
+    return FA_ERR_NULL_POINTER;
+  if (!aligned(P, 16) || !aligned(V, 16) || !aligned(O, 16)) return FA_ERR_UNSUPPORTED;
+  if (!q_rows) return FA_OK;
+  fa::LblParams p = lbl_params(B, Hq, Hkv, Sq, Sk, 1.f, causal);
+  p.p = const_cast<uint16_t*>(static_cast<const uint16_t*>(P));
+  p.v = static_cast<const uint16_t*>(V);
+  p.o = static_cast<uint16_t*>(O);
+  return fa::launch_lbl_pv(p, d_v, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+}
+
+fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
+                           int Sq, int Sk, int d_qk, int d_v, float scale, int causal, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  fa_status_t st = lbl_check_shape(B, Hq, Hkv, Sq, Sk, d_qk, d_v);
+  if (st != FA_OK) return st;
+  const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
+  const bool kv_rows = static_cast<int64_t>(B) * Hkv * Sk > 0;
+  if ((q_rows && (Q == nullptr || O == nullptr)) || (kv_rows && (K == nullptr || V == nullptr)))
+    return FA_ERR_NULL_POINTER;
+  if (!isfinite(scale)) return FA_ERR_BAD_SCALE;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(LSE, 4))
+    return FA_ERR_UNSUPPORTED;
+  if (!q_rows) return FA_OK;
+  // Rows of spill buffer the workspace holds; one block of query rows (or all of Sq if shorter) is
+  // the least a chunk needs.
+  const int64_t row_bytes = lbl_ld(Sk) * 2;
+  const int64_t min_rows = Sq < fa::kLblRows ? Sq : fa::kLblRows;
+  const int64_t cap = row_bytes == 0 ? INT64_MAX : static_cast<int64_t>(workspace_bytes / row_bytes);
+  if (row_bytes > 0 && (workspace == nullptr || cap < min_rows)) return FA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return FA_ERR_UNSUPPORTED;
+
+  fa::LblParams p = lbl_params(B, Hq, Hkv, Sq, Sk, scale, causal);
+  p.q = static_cast<const uint16_t*>(Q);
+  p.k = static_cast<const uint16_t*>(K);
+  p.v = static_cast<const uint16_t*>(V);
+  p.o = static_cast<uint16_t*>(O);
+  p.lse = LSE;
+  p.s = p.p = static_cast<uint16_t*>(workspace);  // probabilities overwrite the scores in place
+  const int n_bh = B * Hq, n_qb = p.nqb;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  auto run = [&](int bh0, int nbh, int qb0, int nqb) {
+    p.bh0 = bh0;
+    p.nbh = nbh;
+    p.qb0 = qb0;
+    p.nqb = nqb;
+    p.xgroup = (bh0 % p.group == 0 && nbh % p.group == 0) ? p.group : 1;
+    const int64_t last = static_cast<int64_t>(qb0 + nqb) * fa::kLblRows;
+    p.rows = static_cast<int64_t>(nbh - 1) * Sq + (last < Sq ? last : Sq) - static_cast<int64_t>(qb0) * fa::kLblRows;
+    if (fa::launch_lbl_scores(p, d_qk, s) != hipSuccess) return false;
+    if (fa::launch_lbl_softmax(p, s) != hipSuccess) return false;
+    return fa::launch_lbl_pv(p, d_v, s) == hipSuccess;
+  };
+  if (cap >= static_cast<int64_t>(Sq)) {
+    // Whole heads per chunk, a multiple of the group size when more than one group fits.
+    int64_t heads = cap / Sq;
+    if (heads > n_bh) heads = n_bh;
+    if (heads >= p.group) heads -= heads % p.group;
+    for (int bh0 = 0; bh0 < n_bh; bh0 += static_cast<int>(heads)) {
+      const int nbh = static_cast<int>(n_bh - bh0 < heads ? n_bh - bh0 : heads);
+      if (!run(bh0, nbh, 0, n_qb)) return FA_ERR_HIP;
+    }
+  } else {
+    // Part of one head per chunk.
+    const int blocks = static_cast<int>(cap / fa::kLblRows);
+    for (int bh = 0; bh < n_bh; ++bh)
+      for (int qb0 = 0; qb0 < n_qb; qb0 += blocks)
+        if (!run(bh, 1, qb0, n_qb - qb0 < blocks ? n_qb - qb0 : blocks)) return FA_ERR_HIP;
+  }
+  return FA_OK;
 }
 
 const char* fa_status_str(fa_status_t s) {

@@ -1,5 +1,6 @@
-// Internal interface between the C-ABI layer (fa_api.hip) and the kernel launchers
-// (fa_fwd_kernel.hip). Not installed; callers use include/fa.h.
+// Internal interface between the C-ABI layer (fa_api.hip) and the kernel launchers (fa_fwd_kernel.hip:
+// fused forward and split mode; fa_lbl_kernel.hip: layer-by-layer operators). Not installed; callers
+// use include/fa.h.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -49,5 +50,42 @@ hipError_t launch_forward(FwdParams p, int d_qk, int d_v, bool causal, hipStream
 // partial results, then the merge pass into O / LSE, both on `stream`. Same requirements as
 // launch_forward plus n_split >= 1 and the partial buffers.
 hipError_t launch_forward_split(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream);
+
+// ---- layer-by-layer (unfused) operators --------------------------------------------------------
+//
+// A work unit is one block of kLblRows query rows of one (batch, query head); bh = b * Hq + h. A chunk
+// is a rectangle of units, query heads bh0 .. bh0+nbh-1 times query blocks qb0 .. qb0+nqb-1, that is
+// either whole heads (qb0 = 0, all blocks) or part of one head (nbh = 1). Row r of the chunk, i.e.
+// (bh - bh0) * Sq + (qb - qb0) * kLblRows + row in block, is row r of the spill buffers S and P
+// (stride ld elements). Key extents are multiples of kLblKeys: the rows of block qb use keys
+// [0, lbl_extent(qb)), the visible keys of the block's last row rounded up.
+constexpr int kLblRows = 128;
+constexpr int kLblKeys = 64;
+// Largest Sk of the layer-by-layer operators: keeps every byte offset inside one block's rows of the
+// spill buffer (kLblRows * ld * 2) below 2^30.
+constexpr int kLblMaxSk = 1 << 22;
+
+struct LblParams {
+  const uint16_t* q;  // bf16 [B][Hq][Sq][d_qk]
+  const uint16_t* k;  // bf16 [B][Hkv][Sk][d_qk]
+  const uint16_t* v;  // bf16 [B][Hkv][Sk][d_v]
+  uint16_t* s;        // bf16 scores of the chunk, row stride ld
+  uint16_t* p;        // bf16 probabilities of the chunk, row stride ld (may equal s)
+  uint16_t* o;        // bf16 [B][Hq][Sq][d_v]
+  float* lse;         // fp32 [B][Hq][Sq] or nullptr
+  int batch, hq, hkv, sq, sk, group, causal;
+  int ld;             // Sk rounded up to kLblKeys
+  float scale;
+  int bh0, nbh, qb0, nqb;
+  int xgroup;         // query heads placed together on one XCD: group if the chunk is aligned to it, else 1
+  int64_t rows;       // rows of the chunk
+};
+
+bool lbl_scores_supported(int d_qk);
+bool lbl_pv_supported(int d_v);
+// Each enqueues one kernel over the chunk on `stream` and returns the launch status.
+hipError_t launch_lbl_scores(const LblParams& p, int d_qk, hipStream_t stream);
+hipError_t launch_lbl_softmax(const LblParams& p, hipStream_t stream);
+hipError_t launch_lbl_pv(const LblParams& p, int d_v, hipStream_t stream);
 
 }  // namespace fa

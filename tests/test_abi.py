@@ -201,3 +201,102 @@ def test_split_parts_heuristic(lib):
     assert fa.fa_fwd_split_parts(256, 1, 1, 1, 64, 96, 96, 0) == 0
     assert fa.fa_fwd_split_parts(0, 1, 1, 1, 64, 64, 64, 0) == 0
     assert fa.fa_fwd_split_parts(256, 1, 0, 1, 64, 64, 64, 0) == 0
+
+
+# ---- layer-by-layer operators: host-side checks only --------------------------------------------
+
+SP = P + 0x20000  # fake, 16-byte aligned spill buffers
+PP = P + 0x40000
+
+
+def call_unfused(**kw):
+    a = dict(Q=QP, K=KP, V=VP, O=OP, LSE=LP, B=1, Hq=4, Hkv=2, Sq=300, Sk=500, d_qk=128, d_v=128,
+             scale=0.125, causal=1, ws=WSP, ws_bytes=None, stream=None)
+    a.update(kw)
+    if a["ws_bytes"] is None:
+        a["ws_bytes"] = fa.fa_lbl_workspace_bytes(max(a["B"], 0), max(a["Hq"], 0), max(a["Sq"], 0), max(a["Sk"], 0))
+    return fa.fa_fwd_unfused(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Sk"],
+                             a["d_qk"], a["d_v"], a["scale"], a["causal"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+def test_lbl_row_stride_and_workspace_bytes(lib):
+    assert [fa.fa_lbl_ld(s) for s in (0, 1, 64, 65, 8192)] == [0, 64, 64, 128, 8192]
+    assert fa.fa_lbl_ld(-1) == -1 and fa.fa_lbl_ld(2**22) == 2**22 and fa.fa_lbl_ld(2**22 + 1) == -1
+    assert fa.fa_lbl_workspace_bytes(2, 3, 5, 100) == 2 * 3 * 5 * 128 * 2
+    for args in ((0, 3, 5, 100), (2, 0, 5, 100), (2, 3, 0, 100), (2, 3, 5, 0), (-1, 3, 5, 100)):
+        assert fa.fa_lbl_workspace_bytes(*args) == 0
+    assert fa.fa_lbl_workspace_bytes(1, 1, 1, 2**22 + 1) == 2**64 - 1
+    assert fa.fa_lbl_workspace_bytes(2**31 - 1, 2**31 - 1, 2**31 - 1, 2**22) == 2**64 - 1
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), fa.FA_ERR_BAD_SHAPE),
+    (dict(Hkv=3), fa.FA_ERR_BAD_SHAPE),
+    (dict(Sk=2**22 + 64), fa.FA_ERR_BAD_SHAPE),
+    (dict(d_qk=96), fa.FA_ERR_UNSUPPORTED),
+    (dict(d_v=192), fa.FA_ERR_UNSUPPORTED),
+    (dict(Q=None), fa.FA_ERR_NULL_POINTER),
+    (dict(V=None), fa.FA_ERR_NULL_POINTER),
+    (dict(scale=float("inf")), fa.FA_ERR_BAD_SCALE),
+    (dict(O=OP + 2), fa.FA_ERR_UNSUPPORTED),
+    (dict(LSE=LP + 2), fa.FA_ERR_UNSUPPORTED),
+    (dict(ws=None), fa.FA_ERR_WORKSPACE),
+    (dict(ws_bytes=128 * 512 * 2 - 1), fa.FA_ERR_WORKSPACE),
+    (dict(ws=WSP + 8), fa.FA_ERR_UNSUPPORTED),
+    # checks in order: shape before dims before pointers before scale before alignment before workspace
+    (dict(Hkv=3, d_qk=96, Q=None), fa.FA_ERR_BAD_SHAPE),
+    (dict(d_qk=96, Q=None, scale=float("nan")), fa.FA_ERR_UNSUPPORTED),
+    (dict(Q=None, scale=float("nan"), ws=None), fa.FA_ERR_NULL_POINTER),
+    (dict(scale=float("nan"), O=OP + 2), fa.FA_ERR_BAD_SCALE),
+    (dict(O=OP + 2, ws=None), fa.FA_ERR_UNSUPPORTED),
+])
+def test_unfused_invalid_arguments_are_rejected_on_host(lib, kw, status):
+    assert call_unfused(**kw) == status
+
+
+def test_unfused_least_workspace_is_accepted_on_host(lib):
+    # one block of 128 rows (all of Sq when shorter) of spill buffer is the least accepted size; the call
+    # would launch, so only the rejection side is exercised here
+    assert call_unfused(ws_bytes=128 * 512 * 2 - 2) == fa.FA_ERR_WORKSPACE
+    assert call_unfused(Sq=50, ws_bytes=50 * 512 * 2 - 2) == fa.FA_ERR_WORKSPACE
+
+
+def test_unfused_empty_problems_need_no_workspace(lib):
+    assert call_unfused(B=0, ws=None, ws_bytes=0) == fa.FA_OK
+    assert call_unfused(Sq=0, Q=None, O=None, ws=None, ws_bytes=0) == fa.FA_OK
+
+
+@pytest.mark.parametrize("name,args,status", [
+    ("scores", dict(Q=None), fa.FA_ERR_NULL_POINTER),
+    ("scores", dict(S=None), fa.FA_ERR_NULL_POINTER),
+    ("scores", dict(d=160), fa.FA_ERR_UNSUPPORTED),
+    ("scores", dict(S=SP + 4), fa.FA_ERR_UNSUPPORTED),
+    ("scores", dict(scale=float("nan")), fa.FA_ERR_BAD_SCALE),
+    ("scores", dict(Sk=2**22 + 1), fa.FA_ERR_BAD_SHAPE),
+    ("softmax", dict(S=None), fa.FA_ERR_NULL_POINTER),
+    ("softmax", dict(P=None), fa.FA_ERR_NULL_POINTER),
+    ("softmax", dict(P=PP + 8), fa.FA_ERR_UNSUPPORTED),
+    ("softmax", dict(Hq=-2), fa.FA_ERR_BAD_SHAPE),
+    ("pv", dict(P=None), fa.FA_ERR_NULL_POINTER),
+    ("pv", dict(V=None), fa.FA_ERR_NULL_POINTER),
+    ("pv", dict(d=192), fa.FA_ERR_UNSUPPORTED),
+    ("pv", dict(Hkv=0), fa.FA_ERR_BAD_SHAPE),
+    # empty problems: nothing to do, no launch
+    ("scores", dict(B=0, Q=None, S=None), fa.FA_OK),
+    ("scores", dict(Sk=0, K=None, S=None), fa.FA_OK),
+    ("softmax", dict(Sq=0, S=None, P=None), fa.FA_OK),
+    ("pv", dict(Hq=0, Hkv=0, P=None, O=None), fa.FA_OK),
+])
+def test_lbl_operators_reject_on_host(lib, name, args, status):
+    a = dict(Q=QP, K=KP, V=VP, O=OP, LSE=LP, S=SP, P=PP, B=1, Hq=4, Hkv=2, Sq=200, Sk=300, d=128, scale=0.1,
+             causal=1, stream=None)
+    a.update(args)
+    if name == "scores":
+        st = fa.fa_lbl_scores(a["Q"], a["K"], a["S"], a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Sk"], a["d"], a["scale"],
+                              a["causal"], a["stream"])
+    elif name == "softmax":
+        st = fa.fa_lbl_softmax(a["S"], a["P"], a["LSE"], a["B"], a["Hq"], a["Sq"], a["Sk"], a["causal"], a["stream"])
+    else:
+        st = fa.fa_lbl_pv(a["P"], a["V"], a["O"], a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Sk"], a["d"], a["causal"],
+                          a["stream"])
+    assert st == status

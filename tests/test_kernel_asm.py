@@ -1,9 +1,14 @@
-"""Static checks of the gfx950 assembly hipcc generates for the attention kernel (no GPU needed).
+"""Static checks of the gfx950 assembly hipcc generates for the kernels (no GPU needed).
 
-The P V MFMAs are written as inline assembly, so the compiler's hazard recognizer does not pad them:
-where the kernel omits the wait states in front of such an MFMA it relies on no VALU instruction
-having written one of its source registers just before. gfx950 needs two wait states between a
-VALU write of a VGPR and an MFMA that reads it; this test checks that in the generated code.
+* The fused kernel's P V MFMAs are written as inline assembly, so the compiler's hazard recognizer
+  does not pad them: where the kernel omits the wait states in front of such an MFMA it relies on no
+  VALU instruction having written one of its source registers just before. gfx950 needs two wait
+  states between a VALU write of a VGPR and an MFMA that reads it; this is checked in the code.
+* Some loads into registers are inline assembly the compiler does not track (Q in the fused kernel,
+  P in the layer-by-layer P V kernel): the kernels order them with explicit vmcnt waits. The check
+  follows every path of each kernel, keeps the queue of vector-memory operations in issue order
+  (vmcnt retires the oldest first) and fails if any instruction touches a register of a load that
+  may still be in flight.
 """
 
 import os
@@ -29,15 +34,24 @@ def _have_hipcc():
 pytestmark = pytest.mark.skipif(not _have_hipcc(), reason="hipcc not installed")
 
 
-@pytest.fixture(scope="module")
-def asm_text():
+def _asm(source):
     d = tempfile.mkdtemp(prefix="fa_asm_")
     try:
         out = os.path.join(d, "kernel.s")
-        fa_build.kernel_asm(out)
+        fa_build.kernel_asm(out, source)
         return open(out).read()
     finally:
         shutil.rmtree(d, ignore_errors=True)
+
+
+@pytest.fixture(scope="module")
+def asm_text():
+    return _asm("fa_fwd_kernel.hip")
+
+
+@pytest.fixture(scope="module")
+def lbl_asm_text():
+    return _asm("fa_lbl_kernel.hip")
 
 
 def _regs(tok):
@@ -54,8 +68,8 @@ def _instructions(text):
     out = []
     for line in text.split("\n"):
         s = line.split(";")[0].strip()
-        if not s or s.startswith("."):
-            continue
+        if not s or (s.startswith(".") and not s.endswith(":")):
+            continue  # directives; local labels (".LBB0_1:") are kept
         out.append(("label", s) if s.endswith(":") else ("ins", s))
     return out
 
@@ -100,3 +114,115 @@ def test_no_scratch(asm_text):
     sizes = re.findall(r"\.amdhsa_private_segment_fixed_size\s+(\d+)", asm_text)
     assert sizes, "no kernel descriptor found"
     assert all(int(x) == 0 for x in sizes), f"kernels use scratch memory: {sizes}"
+
+
+# ---------------------------------------------------------------------------------------------
+# registers of in-flight loads
+# ---------------------------------------------------------------------------------------------
+
+_VMEM = re.compile(r"^(buffer|global|flat)_(load|store|atomic)")
+
+
+def _kernels(text):
+    """{kernel name: [(kind, text, from_inline_asm)]} for every kernel in the assembly, from its entry
+    label to its .Lfunc_end label; kind is "label" or "ins"."""
+    out, cur, in_asm = {}, None, False
+    for line in text.split("\n"):
+        if ";;#ASMSTART" in line:
+            in_asm = True
+        elif ";;#ASMEND" in line:
+            in_asm = False
+        s = line.split(";")[0].strip()
+        if not s or (s.startswith(".") and not s.endswith(":")):
+            continue
+        if s.endswith(":"):
+            if re.fullmatch(r"_Z\w+:", s):
+                cur = out.setdefault(s[:-1], [])
+                continue
+            if s.startswith(".Lfunc_end"):
+                cur = None
+                continue
+            if cur is not None:
+                cur.append(("label", s, False))
+        elif cur is not None:
+            cur.append(("ins", s, in_asm))
+    return out
+
+
+def _operands(s):
+    parts = s.split(None, 1)
+    return [o.strip() for o in parts[1].split(",")] if len(parts) > 1 else []
+
+
+def _in_flight_violations(code):
+    """Flow every reachable (instruction, in-flight queue) state through the kernel's branches;
+    return the instructions that touch a register of an inline-asm load that may still be in
+    flight (the compiler orders its own loads itself; its waits only count those, and untracked
+    operations can only make them stricter). The queue holds every outstanding vector-memory
+    operation in issue order, with the destination registers of inline-asm loads (empty for the
+    rest); vmcnt(N) keeps the newest N. The hardware counter holds at most 63 operations, so older
+    entries are retired, which bounds the states."""
+    labels = {s[:-1]: i for i, (k, s, _) in enumerate(code) if k == "label"}
+    problems, seen = set(), set()
+    work = [(0, ())]
+    while work:
+        i, queue = work.pop()
+        while i < len(code):
+            if (i, queue) in seen:
+                break
+            seen.add((i, queue))
+            kind, s, from_asm = code[i]
+            if kind == "label":
+                i += 1
+                continue
+            op = s.split()[0]
+            ops = _operands(s)
+            if op == "s_endpgm":
+                break
+            if op == "s_waitcnt":
+                m = re.search(r"vmcnt\((\d+)\)", s)
+                if m:
+                    n = int(m.group(1))
+                    queue = queue[len(queue) - n:] if n < len(queue) else queue
+                i += 1
+                continue
+            busy = frozenset().union(*queue)
+            if _VMEM.match(op):
+                is_load = "_load" in op and not s.endswith(" lds")
+                dst = _regs(ops[0]) if is_load else set()
+                srcs = set().union(*(_regs(o) for o in (ops[1:] if is_load else ops)))
+                if (dst | srcs) & busy:
+                    problems.add(s)
+                queue = (queue + (frozenset(dst) if from_asm else frozenset(),))[-63:]
+            elif ops and set().union(*(_regs(o) for o in ops)) & busy:
+                problems.add(s)
+            if op.startswith("s_cbranch") or op == "s_branch":
+                tgt = labels.get(ops[0])
+                assert tgt is not None, f"branch to unknown label: {s}"
+                if op == "s_branch":
+                    i = tgt
+                    continue
+                work.append((tgt, queue))
+            i += 1
+    return sorted(problems)
+
+
+@pytest.mark.parametrize("which", ["fused", "lbl"])
+def test_no_access_to_registers_of_in_flight_loads(which, asm_text, lbl_asm_text):
+    kernels = _kernels(asm_text if which == "fused" else lbl_asm_text)
+    assert kernels, "no kernel found in the assembly"
+    report = {}
+    n_asm_loads = 0
+    for name, code in kernels.items():
+        n_asm_loads += sum(1 for k, t, a in code if a and k == "ins" and re.match(r"(buffer|global)_load", t))
+        bad = _in_flight_violations(code)
+        if bad:
+            report[name] = bad[:5]
+    assert n_asm_loads > 0, "no inline-asm load found: the check would be vacuous"
+    assert not report, "\n".join(f"{k}: {v}" for k, v in report.items())
+
+
+def test_lbl_no_packed_fp32_no_scratch(lbl_asm_text):
+    assert not re.findall(r"\bv_pk_(?:add|mul|fma)_f32\b", lbl_asm_text)
+    sizes = re.findall(r"\.amdhsa_private_segment_fixed_size\s+(\d+)", lbl_asm_text)
+    assert sizes and all(int(x) == 0 for x in sizes), sizes
