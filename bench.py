@@ -17,6 +17,10 @@ JSON line:
 
 Default workload: the Llama-style GQA prefill, B1 Hq32 Hkv8 S8192 d128 causal (config 3). Split mode:
 ``--split N|auto`` with ``--workload decode-128k`` (and the other named decode shapes).
+
+``--unfused`` times the layer-by-layer baseline (scores, mask + softmax, P V with S and P spilled to
+HBM in bf16) on the same workload instead and prints one JSON line with each operator's HBM roofline
+and the fused kernel's time on the same inputs (the paper's layer-by-layer vs. fused comparison).
 """
 
 from __future__ import annotations
@@ -35,7 +39,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2516.6  # 256 CUs x 4096 dense bf16 FLOP/clk/CU x 2.4 GHz
 PEAK_HBM_GBS = 8000.0      # HBM3E
 KERNEL_SOURCES = ["paper_2609_21264_amd/csrc/fa_fwd_kernel.hip", "paper_2609_21264_amd/csrc/fa_api.hip",
-                  "paper_2609_21264_amd/csrc/fa_internal.h"]
+                  "paper_2609_21264_amd/csrc/fa_internal.h", "paper_2609_21264_amd/csrc/fa_device.h"]
 
 
 def kernel_source_hash() -> str:
@@ -182,6 +186,186 @@ def paper_sweep():
                       "rows": rows}), flush=True)
 
 
+def unfused_main(args, w):
+    """The layer-by-layer path on workload w: each operator timed with HIP events on the launch stream
+    (when the whole problem fits one spill buffer), the three-launch step timed by wall clock, and the
+    fused kernel on the same inputs for the ratio. One JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_2609_21264_amd as fa
+    import workloads as W
+    from oracle import bf16_bits_to_f64, lbl_error_bound, naive_attention_rows
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print(f"[bench] unfused, workload: {w.name}", file=sys.stderr, flush=True)
+    q_cpu, k_cpu, v_cpu = W.make_inputs(w)
+    q, k, v = q_cpu.to(dev), k_cpu.to(dev), v_cpu.to(dev)
+    o = torch.empty((w.B, w.Hq, w.Sq, w.dv), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+    handle = torch.cuda.current_stream(dev).cuda_stream
+    stream = torch.cuda.current_stream(dev)
+    full = fa.fa_lbl_workspace_bytes(w.B, w.Hq, w.Sq, w.Sk)
+    cap = int(args.workspace_gib * (1 << 30))
+    ws_bytes = min(full, cap)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    one_chunk = ws_bytes >= full
+    args_common = (w.B, w.Hq, w.Hkv, w.Sq, w.Sk)
+
+    def ok(st):
+        if st != 0:
+            raise fa.FaError(st)
+
+    def op_scores():
+        ok(fa.fa_lbl_scores(q.data_ptr(), k.data_ptr(), ws.data_ptr(), *args_common, w.dqk, w.scale, w.causal,
+                            handle))
+
+    def op_softmax():
+        ok(fa.fa_lbl_softmax(ws.data_ptr(), ws.data_ptr(), lse.data_ptr(), w.B, w.Hq, w.Sq, w.Sk, w.causal, handle))
+
+    def op_pv():
+        ok(fa.fa_lbl_pv(ws.data_ptr(), v.data_ptr(), o.data_ptr(), *args_common, w.dv, w.causal, handle))
+
+    def step_unfused():
+        ok(fa.fa_fwd_unfused(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), *args_common,
+                             w.dqk, w.dv, w.scale, w.causal, ws.data_ptr(), ws_bytes, handle))
+
+    def step_fused():
+        ok(fa.fa_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), o_f.data_ptr(), None, *args_common, w.dqk, w.dv,
+                        w.scale, w.causal, handle))
+
+    o_f = torch.empty_like(o)
+
+    def timed(fn, min_s=0.25, min_n=10, warm_s=0.3):
+        t = time.perf_counter()
+        nw = 0
+        while nw < 3 or time.perf_counter() - t < warm_s:
+            fn()
+            nw += 1
+            torch.cuda.synchronize()
+        per = (time.perf_counter() - t) / nw
+        n = max(min_n, int(min_s / max(per, 1e-6)) + 1)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / n, n, nw
+
+    step_s, steps, warm = timed(step_unfused)
+    print(f"[bench] unfused step {step_s * 1e3:.4f} ms ({steps} timed)", file=sys.stderr, flush=True)
+    fused_s, _, _ = timed(step_fused)
+    print(f"[bench] fused step {fused_s * 1e3:.4f} ms", file=sys.stderr, flush=True)
+
+    kernels = None
+    alg = W.unfused_algorithmic_bytes(w)
+    if one_chunk:
+        # Per operator: events around each launch on the launch stream, over the same number of steps.
+        names = ("scores", "softmax", "pv")
+        evs = {n: [] for n in names}
+        for _ in range(3):
+            op_scores(); op_softmax(); op_pv()
+        torch.cuda.synchronize()
+        for _ in range(steps):
+            for n, fn in zip(names, (op_scores, op_softmax, op_pv)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                fn()
+                b.record(stream)
+                evs[n].append((a, b))
+        torch.cuda.synchronize()
+        kernels = {}
+        for n in names:
+            ms = [a.elapsed_time(b) for a, b in evs[n]]
+            avg = sum(ms) / len(ms)
+            gbs = alg[n] / (avg / 1e3) / 1e9
+            kernels[n] = {"ms": round(avg, 4), "algorithmic_bytes": alg[n], "achieved_gbs": round(gbs, 1),
+                          "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
+        # the output checked below comes from the composite call
+        step_unfused()
+        torch.cuda.synchronize()
+
+    if args.copy_calibration > 0:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: 3 x {args.copy_calibration} MiB device copies", file=sys.stderr, flush=True)
+        del src, dst
+
+    # Parity on sampled rows against exact attention, within the bound of the three bf16 roundings
+    # plus fp32 slack (2^-12 max|V| on O, 2^-12 on LSE).
+    def f64(t):
+        return bf16_bits_to_f64(t.contiguous().view(torch.int16).numpy())
+
+    rows = W.sample_rows(w, n=4, seed_base=3000)
+    res = naive_attention_rows(lambda b, h, r: f64(q_cpu[b, h][r]), lambda b, g: f64(k_cpu[b, g]),
+                               lambda b, g: f64(v_cpu[b, g]), w.B, w.Hq, w.Hkv, w.Sq, w.scale, w.causal, rows)
+    oc, lc = o.cpu(), lse.cpu()
+    worst, worst_lse, n_rows = 0.0, 0.0, 0
+    for idx, (o_ref, l_ref) in enumerate(res):
+        b, h = divmod(idx, w.Hq)
+        g = h // w.group
+        r = rows[idx]
+        s = w.scale * (f64(q_cpu[b, h][r]) @ f64(k_cpu[b, g]).T)
+        if w.causal:
+            s = np.where(np.arange(w.Sk)[None, :] <= r[:, None] + (w.Sk - w.Sq), s, 0.0)
+        m = np.abs(s).max(axis=1) if w.Sk else np.zeros(len(r))
+        vmax = float(np.abs(f64(v_cpu[b, g])).max()) if w.Sk else 0.0
+        bound = lbl_error_bound(m, vmax) + 2.0 ** -12 * vmax
+        err = np.abs(f64(oc[b, h][r]) - o_ref).max(axis=1)
+        worst = max(worst, float((err / np.maximum(bound, 1e-30)).max()))
+        fin = np.isfinite(l_ref)
+        if fin.any():
+            lerr = np.abs(lc[b, h][r].double().numpy()[fin] - l_ref[fin]) / (2.0 ** -8 * m[fin] + 2.0 ** -12)
+            worst_lse = max(worst_lse, float(lerr.max()))
+        n_rows += len(r)
+    parity = {"rows_checked": n_rows, "worst_o_err_over_bound": round(worst, 4),
+              "worst_lse_err_over_bound": round(worst_lse, 4), "pass": bool(worst <= 1 and worst_lse <= 1)}
+    print(f"[bench] parity sample: {parity}", file=sys.stderr, flush=True)
+
+    flops = W.metric_flops(w)
+    total = sum(alg.values())
+    value = flops / step_s / 1e12
+    dominant = max(kernels, key=lambda n: kernels[n]["ms"]) if kernels else None
+    roof = None
+    if kernels:
+        kd = kernels[dominant]
+        roof = {"bound": "hbm", "kernel": f"lbl_{dominant}_kernel", "achieved": kd["achieved_gbs"],
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": kd["frac_of_hbm_peak"], "traffic": None,
+                "kernels": kernels}
+    out = {
+        "metric": "attention fwd GEMM TFLOP/s on 1 MI355X, unfused layer-by-layer path",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(step_s * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Sq": w.Sq, "Sk": w.Sk,
+                   "d_qk": w.dqk, "d_v": w.dv, "causal": w.causal, "path": "unfused",
+                   "spill_buffer_bytes": ws_bytes, "chunks": "one" if one_chunk else "several"},
+        "operational_intensity_flop_per_byte": round(flops / total, 2),
+        "hbm_bound_tflops": round(PEAK_HBM_GBS * 1e9 * flops / total / 1e12, 1),
+        "algorithmic_bytes_per_step": total,
+        "roofline": roof,
+        "fused": {"ms": round(fused_s * 1e3, 4), "tflops": round(flops / fused_s / 1e12, 3),
+                  "algorithmic_bytes": W.algorithmic_bytes(w)},
+        "fused_speedup": round(step_s / fused_s, 3),
+        "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,6 +383,11 @@ def main():
                          "and print one JSON line with a row per shape, in both FLOP conventions")
     ap.add_argument("--split", default=None,
                     help="run split mode (fa_fwd_split) with this many key-range parts, or 'auto'")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time the layer-by-layer baseline (three kernels, S and P spilled) instead, with the "
+                         "fused kernel on the same inputs for comparison")
+    ap.add_argument("--workspace-gib", type=float, default=64.0,
+                    help="largest spill buffer for --unfused (bigger problems run in chunks)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -220,6 +409,9 @@ def main():
     import workloads as W
 
     w = W.EXTRA[args.workload] if args.workload else W.CONFIGS[args.config]
+    if args.unfused:
+        unfused_main(args, w)
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     print(f"[bench] workload {args.config}: {w.name}", file=sys.stderr, flush=True)

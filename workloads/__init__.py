@@ -169,6 +169,28 @@ def algorithmic_bytes(w: Workload, with_lse: bool = True) -> int:
     return 2 * (q + k + v + o) + 4 * lse
 
 
+def visible_scores(w: Workload) -> int:
+    """Number of (query, key) pairs the mask leaves visible: B*Hq*Sq*Sk, or with causal masking the sum
+    over query rows i of clamp(i + 1 + Sk - Sq, 0, Sk)."""
+    if not w.causal:
+        return w.B * w.Hq * w.Sq * w.Sk
+    per_row = np.clip(np.arange(w.Sq, dtype=np.int64) + 1 + w.Sk - w.Sq, 0, w.Sk)
+    return int(w.B * w.Hq * per_row.sum())
+
+
+def unfused_algorithmic_bytes(w: Workload) -> Dict[str, int]:
+    """HBM bytes the layer-by-layer operators must move at minimum, per operator: the score matrix and
+    the probabilities are written once and read once in bf16 over the visible pairs, next to the
+    operators' own inputs and outputs (Q, K for the scores; LSE for the softmax; V, O for P V)."""
+    n = visible_scores(w)
+    q = 2 * w.B * w.Hq * w.Sq * w.dqk
+    k = 2 * w.B * w.Hkv * w.Sk * w.dqk
+    v = 2 * w.B * w.Hkv * w.Sk * w.dv
+    o = 2 * w.B * w.Hq * w.Sq * w.dv
+    lse = 4 * w.B * w.Hq * w.Sq
+    return {"scores": 2 * n + q + k, "softmax": 4 * n + lse, "pv": 2 * n + v + o}
+
+
 def small(name: str, B=1, Hq=1, Hkv=1, Sq=64, Sk=64, dqk=64, dv=64, causal=False,
           scale: Optional[float] = None, seed: int = 7, sigma: float = 1.0) -> Workload:
     """An ad-hoc workload for tests (odd shapes, edge cases)."""
