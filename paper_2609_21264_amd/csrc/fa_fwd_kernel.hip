@@ -116,6 +116,7 @@ struct Cfg {
   // writes a partial result (O normalised by its own row sum, fp32, and its LSE) for a merge pass.
   static constexpr bool SPLIT = SPLIT_;
   static constexpr int NT = NWAVES * 64;
+  static constexpr int WPE = NWAVES > 4 ? NWAVES / 4 : 1;  // waves per SIMD (4 SIMDs per CU)
   static constexpr int BM = NWAVES * 32 * QB;  // query rows per workgroup
   static constexpr int KCH = DQK / 8;          // 16-byte chunks per K-tile row
   static constexpr int VCH = DV / 8;           // 16-byte chunks per V-tile row
@@ -412,7 +413,7 @@ struct Attn {
 };
 
 template <class C>
-__global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(1, 1)))
+__global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(C::WPE, C::WPE)))
 void fa_fwd_kernel(FwdParams p) {
   using A = Attn<C>;
   constexpr int DQK = C::DQK, DV = C::DV, BN = C::BN, QB = C::QB;
