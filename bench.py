@@ -16,7 +16,8 @@ JSON line:
 * parity     -- a few seeded rows per head compared with the oracle (outside the timed region)
 
 Default workload: the Llama-style GQA prefill, B1 Hq32 Hkv8 S8192 d128 causal (config 3). Split mode:
-``--split N|auto`` with ``--workload decode-128k`` (and the other named decode shapes).
+``--split N|auto`` with ``--workload decode-128k`` (and the other named decode shapes); ``--decode``
+runs the decode-shaped path (query heads of a group packed into 32-column blocks) on those shapes.
 
 ``--unfused`` times the layer-by-layer baseline (scores, mask + softmax, P V with S and P spilled to
 HBM in bf16) on the same workload instead and prints one JSON line with each operator's HBM roofline
@@ -383,6 +384,8 @@ def main():
                          "and print one JSON line with a row per shape, in both FLOP conventions")
     ap.add_argument("--split", default=None,
                     help="run split mode (fa_fwd_split) with this many key-range parts, or 'auto'")
+    ap.add_argument("--decode", action="store_true",
+                    help="run the decode-shaped path (fa_fwd_decode; parts from --split, default 'auto')")
     ap.add_argument("--unfused", action="store_true",
                     help="time the layer-by-layer baseline (three kernels, S and P spilled) instead, with the "
                          "fused kernel on the same inputs for comparison")
@@ -423,7 +426,13 @@ def main():
     handle = stream.cuda_stream
 
     n_split = 0
-    if args.split is not None:
+    if args.decode:
+        n_split = (fa.fa_fwd_decode_parts(torch.cuda.get_device_properties(dev).multi_processor_count, w.B, w.Hq,
+                                          w.Hkv, w.Sq, w.Sk)
+                   if args.split in (None, "auto") else int(args.split))
+        ws_bytes = fa.fa_fwd_split_workspace_bytes(w.B, w.Hq, w.Sq, w.dv, n_split)
+        ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)  # allocated before timing
+    elif args.split is not None:
         n_split = (fa.fa_fwd_split_parts(torch.cuda.get_device_properties(dev).multi_processor_count, w.B, w.Hq,
                                          w.Sq, w.Sk, w.dqk, w.dv, w.causal)
                    if args.split == "auto" else int(args.split))
@@ -431,7 +440,11 @@ def main():
         ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)  # allocated before timing
 
     def step():
-        if n_split:
+        if args.decode:
+            st = fa.fa_fwd_decode(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), w.B,
+                                  w.Hq, w.Hkv, w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, n_split, ws.data_ptr(),
+                                  ws_bytes, handle)
+        elif n_split:
             st = fa.fa_fwd_split(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), w.B,
                                  w.Hq, w.Hkv, w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, n_split, ws.data_ptr(),
                                  ws_bytes, handle)
@@ -528,7 +541,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Sq": w.Sq, "Sk": w.Sk,
                    "d_qk": w.dqk, "d_v": w.dv, "causal": w.causal, "scale": w.scale, "seed": w.seed,
-                   "split": n_split or None},
+                   "split": n_split or None, "path": "decode" if args.decode else ("split" if n_split else "fused")},
         "roofline": {**roof,
                      "traffic": traffic,
                      "kernel_ms": {"mean": round(sum(launch_ms) / len(launch_ms), 4), "min": round(min(launch_ms), 4)},

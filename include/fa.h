@@ -122,6 +122,42 @@ fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, f
  * or n_split is <= 0 (nothing to store); SIZE_MAX if the count overflows. */
 size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split);
 
+/*
+ * fa_fwd_decode -- the same operation for decode-shaped problems, where each key/value head has few
+ * query rows (one to a few new tokens per query head; best when (Hq / Hkv) * Sq <= 32). The Hq / Hkv
+ * query heads that share a key/value head and their Sq rows are computed together as the columns of
+ * 32-column matrix-core blocks, so K and V are read once per key/value head and block of 32 rows.
+ * The key range of every (batch, key/value head, block) is cut into n_parts contiguous runs of
+ * 128-key tiles that run as separate
+ * workgroups (the tile-to-tile level, Alg. 2, Sec. 2.1), each running the per-tile online softmax
+ * (Alg. 1); a second kernel merges the parts with the log-sum-exp combination, as fa_fwd_split does.
+ * Results agree with fa_fwd_ex within floating-point rounding.
+ *
+ *   Q .. stream  as in fa_fwd_ex
+ *   n_parts      key-range parts per (batch, key/value head, block), >= 1; parts left without a tile
+ *                contribute nothing. fa_fwd_decode_parts suggests a count.
+ *   workspace    device buffer owned by the caller, 16-byte aligned, at least
+ *                fa_fwd_split_workspace_bytes(B, Hq, Sq, d_v, n_parts) bytes, with the layout of
+ *                fa_fwd_split's workspace; overwritten by the call and not to be touched until the
+ *                call's work on `stream` has completed. NULL only when no byte is needed.
+ *   workspace_bytes  its size in bytes
+ *
+ * Enqueues two kernels on `stream`. Errors: n_parts < 1 (FA_ERR_BAD_SHAPE); then sizes
+ * (FA_ERR_BAD_SHAPE), head dimensions (FA_ERR_UNSUPPORTED), pointers
+ * (FA_ERR_NULL_POINTER), scale (FA_ERR_BAD_SCALE), alignment (FA_ERR_UNSUPPORTED), index ranges
+ * (FA_ERR_BAD_SHAPE); B*Hq*Sq == 0 returns FA_OK without touching the workspace; then more than
+ * 2^31-1 workgroups (FA_ERR_BAD_SHAPE), workspace NULL or too small (FA_ERR_WORKSPACE), workspace not
+ * 16-byte aligned (FA_ERR_UNSUPPORTED).
+ */
+fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
+                          int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
+                          int n_parts, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Suggested n_parts for fa_fwd_decode on a device with n_cu compute units: about one workgroup per
+ * CU in total, no part shorter than 4 key tiles (512 keys), at least 1. Host arithmetic only.
+ * Returns 0 if n_cu, B, Hq, Hkv or Sq <= 0, Hq % Hkv != 0 or Sk < 0. */
+int fa_fwd_decode_parts(int n_cu, int B, int Hq, int Hkv, int Sq, int Sk);
+
 /* Suggested n_split for fa_fwd_split on a device with n_cu compute units: about two workgroups per
  * CU over all parts, no part shorter than 8 key tiles (512 keys), at least 1 (1 means the single
  * pass fa_fwd_ex is the better call). Host arithmetic only, no HIP call. Returns 0 for unsupported

@@ -10,8 +10,10 @@ kernel. The functions below marshal arguments and translate status codes, nothin
 * :func:`fa_lbl_scores`, :func:`fa_lbl_softmax`, :func:`fa_lbl_pv`, :func:`fa_lbl_ld`,
   :func:`fa_lbl_workspace_bytes`, :func:`fa_fwd_unfused` -- the layer-by-layer (unfused) operators
   and their composition, under the same names.
+* :func:`fa_fwd_decode`, :func:`fa_fwd_decode_parts` -- the decode-shaped path (few query rows per
+  key/value head).
 * :func:`forward` -- convenience wrapper over torch tensors (``n_split`` > 1 selects split mode and
-  takes the workspace from torch's allocator).
+  takes the workspace from torch's allocator; ``decode=True`` the decode-shaped path).
 * :func:`forward_unfused` -- the same over the unfused path (``fa_fwd_unfused``).
 """
 
@@ -26,7 +28,8 @@ from ._lib import (FA_ERR_BAD_SCALE, FA_ERR_BAD_SHAPE, FA_ERR_HIP, FA_ERR_NULL_P
 
 __all__ = ["fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
            "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
-           "fa_lbl_workspace_bytes", "fa_fwd_unfused", "forward", "forward_unfused", "FaError", "LIB_PATH"]
+           "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts", "forward",
+           "forward_unfused", "FaError", "LIB_PATH"]
 
 
 class FaError(RuntimeError):
@@ -75,6 +78,19 @@ def fa_fwd_split_parts(n_cu: int, B: int, Hq: int, Sq: int, Sk: int, d_qk: int, 
     """C ``fa_fwd_split_parts``."""
     return int(_lib.load().fa_fwd_split_parts(int(n_cu), int(B), int(Hq), int(Sq), int(Sk), int(d_qk), int(d_v),
                                               int(bool(causal))))
+
+
+def fa_fwd_decode(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, Hq: int, Hkv: int, Sq: int,
+                  Sk: int, d_qk: int, d_v: int, scale: float, causal: bool, n_parts: int, workspace: Optional[int],
+                  workspace_bytes: int, stream: int) -> int:
+    """C ``fa_fwd_decode``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_fwd_decode(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, float(scale),
+                                         int(bool(causal)), int(n_parts), workspace, int(workspace_bytes), stream))
+
+
+def fa_fwd_decode_parts(n_cu: int, B: int, Hq: int, Hkv: int, Sq: int, Sk: int) -> int:
+    """C ``fa_fwd_decode_parts``."""
+    return int(_lib.load().fa_fwd_decode_parts(int(n_cu), int(B), int(Hq), int(Hkv), int(Sq), int(Sk)))
 
 
 def fa_lbl_scores(Q: int, K: int, S: int, B: int, Hq: int, Hkv: int, Sq: int, Sk: int, d_qk: int, scale: float,
@@ -167,15 +183,17 @@ def forward_unfused(q, k, v, causal: bool = False, scale: Optional[float] = None
 
 
 def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return_lse: bool = False,
-            out=None, lse=None, stream=None, n_split=1):
+            out=None, lse=None, stream=None, n_split=1, decode: bool = False):
     """Attention forward over contiguous bf16 BHSD torch tensors on one GPU.
 
     q [B, Hq, Sq, d_qk], k [B, Hkv, Sk, d_qk], v [B, Hkv, Sk, d_v]; returns O [B, Hq, Sq, d_v] (bf16)
     and, with ``return_lse``, LSE [B, Hq, Sq] (float32, natural log). ``scale`` defaults to
     1/sqrt(d_qk). ``n_split`` > 1 runs split mode (``fa_fwd_split``) with that many key-range parts
     per query block and a workspace from torch's allocator; ``n_split="auto"`` takes the count
-    ``fa_fwd_split_parts`` suggests for the device. The kernels are enqueued on ``stream``
-    (default: torch's current stream); the call does not synchronise.
+    ``fa_fwd_split_parts`` suggests for the device. ``decode=True`` runs the decode-shaped path
+    (``fa_fwd_decode``, for few query rows per key/value head) with ``n_split`` parts ("auto":
+    ``fa_fwd_decode_parts``). The kernels are enqueued on ``stream`` (default: torch's current
+    stream); the call does not synchronise.
     """
     import torch
 
@@ -209,6 +227,22 @@ def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return
         stream = torch.cuda.current_stream(q.device)
     handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
     name = "fa_fwd_ex"
+    if decode:
+        n_cu = torch.cuda.get_device_properties(q.device).multi_processor_count
+        parts = fa_fwd_decode_parts(n_cu, B, Hq, Hkv, Sq, Sk) if n_split == "auto" else int(n_split)
+        with torch.cuda.device(q.device):
+            nbytes = fa_fwd_split_workspace_bytes(B, Hq, Sq, dv, parts)
+            ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+            if isinstance(stream, torch.cuda.Stream):
+                ws.record_stream(stream)
+            st = fa_fwd_decode(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                               lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, dqk, dv, scale, causal,
+                               parts, ws.data_ptr(), nbytes, handle)
+        if st != FA_OK:
+            if st in (FA_ERR_NULL_POINTER, FA_ERR_BAD_SHAPE, FA_ERR_UNSUPPORTED, FA_ERR_BAD_SCALE, FA_ERR_WORKSPACE):
+                raise ValueError(f"fa_fwd_decode rejected the arguments: {fa_status_str(st)}")
+            raise FaError(st)
+        return (out, lse) if return_lse else out
     if n_split == "auto":
         n_cu = torch.cuda.get_device_properties(q.device).multi_processor_count
         n_split = fa_fwd_split_parts(n_cu, B, Hq, Sq, Sk, dqk, dv, causal)

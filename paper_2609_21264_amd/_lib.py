@@ -24,7 +24,7 @@ FA_ERR_WORKSPACE = 6
 #: Symbols include/fa.h declares.
 EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
             "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
-            "fa_lbl_workspace_bytes", "fa_fwd_unfused")
+            "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts")
 
 _lib = None
 
@@ -67,5 +67,9 @@ def load() -> ctypes.CDLL:
     lib.fa_lbl_workspace_bytes.restype = ctypes.c_size_t
     lib.fa_fwd_unfused.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, vp, ctypes.c_size_t, vp]
     lib.fa_fwd_unfused.restype = i
+    lib.fa_fwd_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, i, vp, ctypes.c_size_t, vp]
+    lib.fa_fwd_decode.restype = i
+    lib.fa_fwd_decode_parts.argtypes = [i, i, i, i, i, i]
+    lib.fa_fwd_decode_parts.restype = i
     _lib = lib
     return lib

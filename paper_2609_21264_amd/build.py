@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libfa.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-SOURCES = ["fa_api.hip", "fa_fwd_kernel.hip", "fa_lbl_kernel.hip"]
+SOURCES = ["fa_api.hip", "fa_fwd_kernel.hip", "fa_lbl_kernel.hip", "fa_decode_kernel.hip"]
 ARCH = "gfx950"
 
 

@@ -149,6 +149,68 @@ fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, f
                  workspace_bytes);
 }
 
+fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
+                          int Sq, int Sk, int d_qk, int d_v, float scale, int causal, int n_parts, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  if (n_parts < 1) return FA_ERR_BAD_SHAPE;
+  if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0) return FA_ERR_BAD_SHAPE;
+  if (Hq > 0 && (Hkv <= 0 || Hq % Hkv != 0)) return FA_ERR_BAD_SHAPE;
+  if (fa::block_rows(d_qk, d_v, causal != 0) == 0) return FA_ERR_UNSUPPORTED;
+  const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
+  const bool kv_rows = static_cast<int64_t>(B) * Hkv * Sk > 0;
+  if ((q_rows && (Q == nullptr || O == nullptr)) || (kv_rows && (K == nullptr || V == nullptr)))
+    return FA_ERR_NULL_POINTER;
+  if (!isfinite(scale)) return FA_ERR_BAD_SCALE;
+  const double c = fabs(static_cast<double>(scale)) * 1.4426950408889634074;
+  if (c > FLT_MAX) return FA_ERR_BAD_SCALE;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(LSE, 4))
+    return FA_ERR_UNSUPPORTED;
+  const int64_t dmax = d_qk > d_v ? d_qk : d_v;
+  if (static_cast<int64_t>(Sq) * dmax > INT_MAX || static_cast<int64_t>(Sk) * dmax > INT_MAX) return FA_ERR_BAD_SHAPE;
+  if (!q_rows) return FA_OK;
+  const int64_t n_cb = (static_cast<int64_t>(Hq / Hkv) * Sq + 31) / 32;
+  if (static_cast<int64_t>(B) * Hkv * n_cb * n_parts > INT_MAX || static_cast<int64_t>(B) * Hq > INT_MAX)
+    return FA_ERR_BAD_SHAPE;
+  const int64_t need = split_workspace_bytes(B, Hq, Sq, d_v, n_parts);
+  if (need < 0 || workspace == nullptr || static_cast<uint64_t>(need) > workspace_bytes) return FA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return FA_ERR_UNSUPPORTED;
+
+  fa::DecodeParams p{};
+  p.q = static_cast<const uint16_t*>(Q);
+  p.k = static_cast<const uint16_t*>(K);
+  p.v = static_cast<const uint16_t*>(V);
+  p.o = static_cast<uint16_t*>(O);
+  p.lse = LSE;
+  p.batch = B;
+  p.hq = Hq;
+  p.hkv = Hkv;
+  p.sq = Sq;
+  p.sk = Sk;
+  p.group = Hq / Hkv;
+  p.causal = causal != 0;
+  const float cmag = c < FLT_MIN ? FLT_MIN : static_cast<float>(c);
+  p.cs = scale < 0.f ? -cmag : cmag;
+  p.rows = p.group * Sq;
+  p.n_parts = n_parts;
+  const int64_t rows = static_cast<int64_t>(B) * Hq * Sq;
+  p.o_part = static_cast<float*>(workspace);
+  p.lse_part = p.o_part + rows * n_parts * d_v;
+  return fa::launch_decode(p, d_qk, d_v, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+}
+
+int fa_fwd_decode_parts(int n_cu, int B, int Hq, int Hkv, int Sq, int Sk) {
+  if (n_cu <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || Sq <= 0 || Sk < 0) return 0;
+  // One workgroup per CU in total (a workgroup holds two K+V tiles in LDS, so one fits a CU), but
+  // no part shorter than 4 key tiles.
+  const int64_t n_cb = (static_cast<int64_t>(Hq / Hkv) * Sq + 31) / 32;
+  const int64_t items = static_cast<int64_t>(B) * Hkv * n_cb;
+  const int64_t tiles = (static_cast<int64_t>(Sk) + fa::decode_tile_keys() - 1) / fa::decode_tile_keys();
+  int64_t parts = (n_cu + items - 1) / items;
+  const int64_t max_parts = (tiles + 3) / 4;
+  if (parts > max_parts) parts = max_parts;
+  return parts < 1 ? 1 : static_cast<int>(parts);
+}
+
 int fa_fwd_split_parts(int n_cu, int B, int Hq, int Sq, int Sk, int d_qk, int d_v, int causal) {
   const int bm = fa::block_rows(d_qk, d_v, causal != 0);
   if (bm == 0 || n_cu <= 0 || B <= 0 || Hq <= 0 || Sq <= 0 || Sk < 0) return 0;

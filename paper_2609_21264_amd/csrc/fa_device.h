@@ -52,6 +52,18 @@ __device__ __forceinline__ T bit_cast(const U& u) {
   return __builtin_bit_cast(T, u);
 }
 
+// max / sum of a per-lane value with the value of the lane 32 positions away. After
+// permlane32_swap(x, x) the two results hold {own, partner} in some order on every lane, and both
+// reductions are symmetric.
+__device__ __forceinline__ float half_swap_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_swap_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   f32x2 f = {lo, hi};
   return bit_cast<uint32_t>(__builtin_convertvector(f, bf16x2));  // v_cvt_pk_bf16_f32, RNE

@@ -68,18 +68,6 @@ __device__ __forceinline__ int o_swizzle(int r) { return DV >= 128 ? (r & 15) : 
 template <int DV>
 __device__ __forceinline__ int o_half(int r) { return DV >= 128 ? ((r ^ (r >> 4)) & 1) : (((r >> 1) ^ (r >> 4)) & 1); }
 
-// max / sum of a per-lane value with the value of the lane 32 positions away. After
-// permlane32_swap(x, x) the two results hold {own, partner} in some order on every lane, and both
-// reductions are symmetric.
-__device__ __forceinline__ float half_swap_max(float x) {
-  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float half_swap_sum(float x) {
-  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 // The P V product is issued through inline asm so that its accumulators O stay in AGPRs for the
 // whole kernel (the score product uses the builtin; its accumulators are VGPRs). The compiler does
 // not model hazards of inline asm, so:
@@ -769,6 +757,15 @@ hipError_t launch_forward(FwdParams p, int d_qk, int d_v, bool causal, hipStream
   return launch_dims<false>(p, d_qk, d_v, causal, stream);
 }
 
+hipError_t launch_merge(MergeParams m, int d_v, hipStream_t stream) {
+  const int64_t threads = m.rows * (d_v / 4);
+  const dim3 grid((unsigned)((threads + 255) / 256));
+  void* args[] = {&m};
+  const void* k = d_v == 64 ? reinterpret_cast<const void*>(&fa_merge_kernel<64>)
+                            : reinterpret_cast<const void*>(&fa_merge_kernel<128>);
+  return hipLaunchKernel(k, grid, dim3(256), args, 0, stream);
+}
+
 hipError_t launch_forward_split(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream) {
   const hipError_t e = launch_dims<true>(p, d_qk, d_v, causal, stream);
   if (e != hipSuccess) return e;
@@ -779,12 +776,7 @@ hipError_t launch_forward_split(FwdParams p, int d_qk, int d_v, bool causal, hip
   m.lse = p.lse;
   m.rows = (int64_t)p.batch * p.hq * p.sq;
   m.n_split = p.n_split;
-  const int64_t threads = m.rows * (d_v / 4);
-  const dim3 grid((unsigned)((threads + 255) / 256));
-  void* args[] = {&m};
-  const void* k = d_v == 64 ? reinterpret_cast<const void*>(&fa_merge_kernel<64>)
-                            : reinterpret_cast<const void*>(&fa_merge_kernel<128>);
-  return hipLaunchKernel(k, grid, dim3(256), args, 0, stream);
+  return launch_merge(m, d_v, stream);
 }
 
 }  // namespace fa

@@ -51,6 +51,38 @@ hipError_t launch_forward(FwdParams p, int d_qk, int d_v, bool causal, hipStream
 // launch_forward plus n_split >= 1 and the partial buffers.
 hipError_t launch_forward_split(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream);
 
+// The merge pass alone (d_v 64 or 128), on `stream`.
+hipError_t launch_merge(MergeParams m, int d_v, hipStream_t stream);
+
+// ---- decode-shaped problems (fa_decode_kernel.hip) -----------------------------------------------
+//
+// The group's query heads and their Sq rows form the columns of 32-column MFMA blocks; workgroup t
+// takes part t % n_parts of column block (t / n_parts) % n_cb of (batch, key/value head)
+// t / (n_parts * n_cb), and the parts are
+// merged by the merge pass of split mode (same partial-result layout: o_part fp32
+// [n_parts][B][Hq][Sq][d_v], lse_part fp32 [n_parts][B][Hq][Sq]).
+struct DecodeParams {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* lse;
+  float* o_part;
+  float* lse_part;
+  int batch, hq, hkv, sq, sk, group, causal;
+  float cs;           // scale * log2(e), as in FwdParams
+  int rows;           // group * Sq (columns)
+  int n_parts;
+  int n_tiles, per;   // filled by launch_decode: key tiles, tiles per part
+  int n_cb;           // filled by launch_decode: 32-column blocks
+  int64_t total_rows; // B * Hq * Sq, filled by launch_decode
+};
+
+// Keys per tile of the decode kernel.
+int decode_tile_keys();
+// Enqueue the decode kernel and the merge pass on `stream`; (d_qk, d_v) in {(64,64), (128,128), (192,128)}.
+hipError_t launch_decode(DecodeParams p, int d_qk, int d_v, hipStream_t stream);
+
 // ---- layer-by-layer (unfused) operators --------------------------------------------------------
 //
 // A work unit is one block of kLblRows query rows of one (batch, query head); bh = b * Hq + h. A chunk

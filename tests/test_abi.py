@@ -300,3 +300,53 @@ def test_lbl_operators_reject_on_host(lib, name, args, status):
         st = fa.fa_lbl_pv(a["P"], a["V"], a["O"], a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Sk"], a["d"], a["causal"],
                           a["stream"])
     assert st == status
+
+
+# ---- decode-shaped path: host-side checks only ----------------------------------------------------
+
+def call_decode(**kw):
+    a = dict(Q=QP, K=KP, V=VP, O=OP, LSE=LP, B=1, Hq=32, Hkv=8, Sq=1, Sk=4096, d_qk=128, d_v=128,
+             scale=0.125, causal=0, n_parts=4, ws=WSP, ws_bytes=None, stream=None)
+    a.update(kw)
+    if a["ws_bytes"] is None:
+        a["ws_bytes"] = fa.fa_fwd_split_workspace_bytes(max(a["B"], 0), max(a["Hq"], 0), max(a["Sq"], 0),
+                                                        max(a["d_v"], 0), max(a["n_parts"], 0))
+    return fa.fa_fwd_decode(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Sk"],
+                            a["d_qk"], a["d_v"], a["scale"], a["causal"], a["n_parts"], a["ws"], a["ws_bytes"],
+                            a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_parts=0), fa.FA_ERR_BAD_SHAPE),
+    (dict(n_parts=0, Q=None), fa.FA_ERR_BAD_SHAPE),
+    (dict(Hkv=5), fa.FA_ERR_BAD_SHAPE),
+    (dict(d_qk=96, d_v=96), fa.FA_ERR_UNSUPPORTED),
+    (dict(K=None), fa.FA_ERR_NULL_POINTER),
+    (dict(scale=float("nan")), fa.FA_ERR_BAD_SCALE),
+    (dict(V=VP + 4), fa.FA_ERR_UNSUPPORTED),
+    (dict(Sk=20_000_000), fa.FA_ERR_BAD_SHAPE),
+    (dict(ws=None), fa.FA_ERR_WORKSPACE),
+    (dict(ws_bytes=64), fa.FA_ERR_WORKSPACE),
+    (dict(ws=WSP + 4), fa.FA_ERR_UNSUPPORTED),
+    (dict(B=1, Hq=4096, Hkv=4096, Sq=1, n_parts=2 ** 20), fa.FA_ERR_BAD_SHAPE),
+])
+def test_decode_invalid_arguments_are_rejected_on_host(lib, kw, status):
+    assert call_decode(**kw) == status
+
+
+def test_decode_empty_problems_need_no_workspace(lib):
+    assert call_decode(B=0, ws=None, ws_bytes=0) == fa.FA_OK
+    assert call_decode(Sq=0, Q=None, O=None, ws=None, ws_bytes=0) == fa.FA_OK
+
+
+def test_decode_parts_heuristic(lib):
+    # 8 key/value heads, one 32-column block each, 1024 tiles of 128 keys: 32 parts (one workgroup per CU)
+    assert fa.fa_fwd_decode_parts(256, 1, 32, 8, 1, 131072) == 32
+    # 16 rows per query head, 4 heads per group: two column blocks -> 16 parts
+    assert fa.fa_fwd_decode_parts(256, 1, 32, 8, 16, 131072) == 16
+    # few tiles cap the parts at 4 tiles each
+    assert fa.fa_fwd_decode_parts(256, 1, 32, 8, 1, 1024) == 2
+    assert fa.fa_fwd_decode_parts(256, 1, 32, 8, 1, 100) == 1
+    for args in ((0, 1, 32, 8, 1, 100), (256, 0, 32, 8, 1, 100), (256, 1, 32, 5, 1, 100), (256, 1, 32, 8, 0, 100),
+                 (256, 1, 32, 8, 1, -1)):
+        assert fa.fa_fwd_decode_parts(*args) == 0

@@ -54,6 +54,11 @@ def lbl_asm_text():
     return _asm("fa_lbl_kernel.hip")
 
 
+@pytest.fixture(scope="module")
+def decode_asm_text():
+    return _asm("fa_decode_kernel.hip")
+
+
 def _regs(tok):
     m = re.fullmatch(r"([va])\[(\d+):(\d+)\]", tok)
     if m:
@@ -222,7 +227,22 @@ def test_no_access_to_registers_of_in_flight_loads(which, asm_text, lbl_asm_text
     assert not report, "\n".join(f"{k}: {v}" for k, v in report.items())
 
 
-def test_lbl_no_packed_fp32_no_scratch(lbl_asm_text):
-    assert not re.findall(r"\bv_pk_(?:add|mul|fma)_f32\b", lbl_asm_text)
-    sizes = re.findall(r"\.amdhsa_private_segment_fixed_size\s+(\d+)", lbl_asm_text)
+@pytest.mark.parametrize("which", ["lbl", "decode"])
+def test_other_kernels_no_packed_fp32_no_scratch(which, lbl_asm_text, decode_asm_text):
+    text = lbl_asm_text if which == "lbl" else decode_asm_text
+    assert not re.findall(r"\bv_pk_(?:add|mul|fma)_f32\b", text)
+    sizes = re.findall(r"\.amdhsa_private_segment_fixed_size\s+(\d+)", text)
     assert sizes and all(int(x) == 0 for x in sizes), sizes
+
+
+def test_decode_no_access_to_registers_of_in_flight_loads(decode_asm_text):
+    kernels = _kernels(decode_asm_text)
+    assert kernels
+    report = {n: bad[:5] for n, code in kernels.items() if (bad := _in_flight_violations(code))}
+    assert not report, report
+
+
+def test_no_scalar_memory_writes(asm_text, lbl_asm_text, decode_asm_text):
+    # Every store and atomic goes through the vector memory path.
+    for text in (asm_text, lbl_asm_text, decode_asm_text):
+        assert not re.findall(r"\bs_(?:store|atomic|buffer_store|dcache_wb|dcache_discard)\w*", text)
