@@ -9,13 +9,14 @@
 // (Hq / Hkv) * Sq <= 32), so K and V are read once per key/value head and column block, and the work
 // per key is one 32-column block:
 //  * A workgroup (4 waves) takes one key range ("part") of one column block of one (batch, key/value
-//    head). Key tiles of 128 rows go HBM -> LDS through direct-to-LDS loads, one tile ahead in a
-//    two-slot ring; wave w handles keys 32w .. 32w + 31 of each tile.
+//    head). Key tiles of 128 rows go HBM -> LDS through direct-to-LDS loads in a two-slot ring; wave w
+//    loads and handles keys 32w .. 32w + 31 of each tile, so the waves run their rings without
+//    barriers, and each issues tile j+1 before waiting for tile j (two tiles in flight).
 //  * Per wave and tile: S^T = K Q^T (v_mfma_f32_32x32x16_bf16, Q resident as the B operand, K rows
 //    in the permuted order perm32), the mask, the exact tile maximum of every column, the rescale of
 //    the running sum and of O, P = 2^(s - m) rounded to bf16 in place as the B operand of
 //    O^T += V^T P^T (V read with ds_read_b64_tr_b16).
-//  * The four waves' (m, l, O) are combined through LDS (log-sum-exp weights) and the workgroup writes
+//  * The waves' (m, l, O) are combined through LDS (log-sum-exp weights) and the workgroup writes
 //    its part's O, normalised by the part's own sum, and the part's LSE; the merge kernel of split mode
 //    combines the parts.
 #include <hip/hip_runtime.h>
@@ -28,8 +29,15 @@
 namespace fa {
 namespace {
 
-constexpr int kDecWaves = 4;
+#ifndef FA_DEC_WAVES
+#define FA_DEC_WAVES 4
+#endif
+#ifndef FA_DEC_SLOTS
+#define FA_DEC_SLOTS 2
+#endif
+constexpr int kDecWaves = FA_DEC_WAVES;   // waves per workgroup, 32 keys of each tile per wave
 constexpr int kDecKeys = kDecWaves * 32;  // keys per tile
+constexpr int kDecSlots = FA_DEC_SLOTS;   // ring slots: tile j + kDecSlots - 1 is loaded from step j on
 
 template <int DQK, int DV>
 struct DecCfg {
@@ -39,7 +47,7 @@ struct DecCfg {
   static constexpr int K_BYTES = kDecKeys * DQK * 2;
   static constexpr int V_BYTES = kDecKeys * DV * 2;
   static constexpr int SLOT = K_BYTES + V_BYTES;
-  static constexpr int LDS_BYTES = 2 * SLOT;
+  static constexpr int LDS_BYTES = kDecSlots * SLOT;
   static constexpr int K_LOADS = kDecKeys * KCH / 64 / kDecWaves;  // direct-to-LDS loads per wave per tile
   static constexpr int V_LOADS = kDecKeys * VCH / 64 / kDecWaves;
   // Cross-wave combination: every wave's O^T as [32 columns][DV + 4] fp32 (the 16-byte pad puts
@@ -48,7 +56,10 @@ struct DecCfg {
   static constexpr int O_BYTES = kDecWaves * 32 * OROW * 4;
   static_assert(O_BYTES + 2 * kDecWaves * 32 * 4 <= LDS_BYTES, "combination buffers fit in the ring");
   static_assert(LDS_BYTES <= 163840, "LDS budget");
-  static_assert(K_LOADS + V_LOADS < 64, "vmcnt range");
+  static_assert(V_LOADS + (kDecSlots - 1) * (K_LOADS + V_LOADS) < 64 && kDecSlots >= 2, "vmcnt range");
+  // Wave w's share of each tile's loads is exactly its own 32 K and V rows, so the waves never read
+  // each other's LDS data in the loop (no barrier there).
+  static_assert(K_LOADS * 64 == 32 * KCH && V_LOADS * 64 == 32 * VCH, "wave-private tile rows");
 };
 
 template <int DQK, int DV>
@@ -92,8 +103,8 @@ void fa_decode_kernel(DecodeParams p) {
   TileLoader<kDecWaves, kDecKeys, C::VCH> vload;
   kload.init(kh, k_end, wave, lane, [](int r) { return k_swizzle<DQK>(r); });
   vload.init(vh, k_end, wave, lane, [](int r) { return v_swizzle<DV>(r); });
-  auto kslot = [&](int t) { return smem + (t & 1) * C::SLOT; };
-  auto vslot = [&](int t) { return smem + (t & 1) * C::SLOT + C::K_BYTES; };
+  auto kslot = [&](int t) { return smem + (t % kDecSlots) * C::SLOT; };
+  auto vslot = [&](int t) { return smem + (t % kDecSlots) * C::SLOT + C::K_BYTES; };
   // Lane constants of the V transpose read (as in the prefill kernel).
   const int v_key = 8 * (lane >> 5) + ((lane & 15) >> 2);
   const int v_t = (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) ^ v_swizzle<DV>(v_key);
@@ -104,18 +115,24 @@ void fa_decode_kernel(DecodeParams p) {
   for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  // Per wave: tile 0's loads, then per step j the loads of tile j+1 (after the barrier that frees its
-  // slot). Before step j only tile j's loads are outstanding.
-  kload.issue(t0 * kDecKeys, kslot(0), wave);
-  vload.issue(t0 * kDecKeys, vslot(0), wave);
+  // Each wave loads and reads only its own rows of every tile (see DecCfg), so it runs its ring on
+  // its own: the loads of tiles 0 .. D-1 (D = slots - 1) first, then at the start of step j those of
+  // tile j+D into the slot of tile j-1, which this wave has finished reading. Step j then waits for
+  // K(j) (issued after it: V(j) and the D tiles after j) before the scores and for V(j) before P V.
+  constexpr int D = kDecSlots - 1;
+  constexpr int L = C::K_LOADS + C::V_LOADS;
+#pragma unroll
+  for (int t = 0; t < D; ++t) {
+    kload.issue((t0 + t) * kDecKeys, kslot(t), wave);
+    vload.issue((t0 + t) * kDecKeys, vslot(t), wave);
+  }
   for (int j = 0; j < nt; ++j) {
     compiler_fence();
-    wait_vmcnt<0>();
+    kload.issue((t0 + j + D) * kDecKeys, kslot(j + D), wave);
+    vload.issue((t0 + j + D) * kDecKeys, vslot(j + D), wave);
     compiler_fence();
-    __builtin_amdgcn_s_barrier();
+    wait_vmcnt<C::V_LOADS + D * L>();
     compiler_fence();
-    kload.issue((t0 + j + 1) * kDecKeys, kslot(j + 1), wave);
-    vload.issue((t0 + j + 1) * kDecKeys, vslot(j + 1), wave);
     const unsigned char* sK = kslot(j);
     const unsigned char* sV = vslot(j);
     const int n0 = (t0 + j) * kDecKeys + 32 * wave;  // first key of this wave's block
@@ -153,6 +170,9 @@ void fa_decode_kernel(DecodeParams p) {
     l_run = l_run * alpha + rs;
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+    compiler_fence();
+    wait_vmcnt<D * L>();  // V(j)
+    compiler_fence();
     // O^T += V^T P^T over the wave's 32 keys in two 16-key k-steps; P of keys 16 ps + 8 h .. +7 is
     // registers 8 ps .. 8 ps + 7.
 #pragma unroll
@@ -193,8 +213,9 @@ void fa_decode_kernel(DecodeParams p) {
           f32x4{oacc[db][4 * g4], oacc[db][4 * g4 + 1], oacc[db][4 * g4 + 2], oacc[db][4 * g4 + 3]};
   __syncthreads();
 
-  // Each thread finishes DV / 8 dims of one column: 8 threads per column, 32 columns.
-  const int col = tid >> 3, d0 = (tid & 7) * (DV / 8);
+  // Each thread finishes DV / TPC dims of one column: TPC threads per column, 32 columns.
+  constexpr int TPC = kDecWaves * 64 / 32;
+  const int col = tid / TPC, d0 = (tid % TPC) * (DV / TPC);
   if (c0 + col < p.rows) {
     float mw[kDecWaves], M = -INFINITY;
 #pragma unroll
@@ -213,14 +234,14 @@ void fa_decode_kernel(DecodeParams p) {
     const int64_t orow_g = ((int64_t)b * p.hq + g * p.group + cm) * p.sq + ci;
     float* dst = p.o_part + ((int64_t)part * p.total_rows + orow_g) * DV + d0;
 #pragma unroll
-    for (int d = 0; d < DV / 8; d += 4) {
+    for (int d = 0; d < DV / TPC; d += 4) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int w = 0; w < kDecWaves; ++w)
         acc += wt[w] * *reinterpret_cast<const f32x4*>(ob + (w * 32 + col) * C::OROW + d0 + d);
       *reinterpret_cast<f32x4*>(dst + d) = acc * inv;
     }
-    if ((tid & 7) == 0) p.lse_part[(int64_t)part * p.total_rows + orow_g] = L > 0.f ? (M + log2f(L)) * 0.69314718055994530942f : -INFINITY;
+    if (tid % TPC == 0) p.lse_part[(int64_t)part * p.total_rows + orow_g] = L > 0.f ? (M + log2f(L)) * 0.69314718055994530942f : -INFINITY;
   }
 }
 
