@@ -111,8 +111,8 @@ fa_status_t fa_fwd_ex(const void* Q, const void* K, const void* V, void* O, floa
  *
  * Enqueues two kernels on `stream`. Errors: n_split < 1 first (FA_ERR_BAD_SHAPE), then the checks of
  * fa_fwd_ex in their order (a degenerate size still returns FA_OK without touching the workspace),
- * then more than 2^31-1 workgroups in total (FA_ERR_BAD_SHAPE), workspace NULL or too small
- * (FA_ERR_WORKSPACE), workspace not 16-byte aligned (FA_ERR_UNSUPPORTED).
+ * then more than 2^31-1 workgroups in total or more than 2^31-1 rows B*Hq*Sq (FA_ERR_BAD_SHAPE),
+ * workspace NULL or too small (FA_ERR_WORKSPACE), workspace not 16-byte aligned (FA_ERR_UNSUPPORTED).
  */
 fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
                          int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
@@ -146,8 +146,8 @@ size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split)
  * (FA_ERR_BAD_SHAPE), head dimensions (FA_ERR_UNSUPPORTED), pointers
  * (FA_ERR_NULL_POINTER), scale (FA_ERR_BAD_SCALE), alignment (FA_ERR_UNSUPPORTED), index ranges
  * (FA_ERR_BAD_SHAPE); B*Hq*Sq == 0 returns FA_OK without touching the workspace; then more than
- * 2^31-1 workgroups (FA_ERR_BAD_SHAPE), workspace NULL or too small (FA_ERR_WORKSPACE), workspace not
- * 16-byte aligned (FA_ERR_UNSUPPORTED).
+ * 2^31-1 workgroups or 2^31-1 rows B*Hq*Sq (FA_ERR_BAD_SHAPE), workspace NULL or too small
+ * (FA_ERR_WORKSPACE), workspace not 16-byte aligned (FA_ERR_UNSUPPORTED).
  */
 fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
                           int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,

@@ -52,6 +52,7 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
     return FA_ERR_BAD_SHAPE;
   if (n_split > 0) {
     if (n_wg * n_split > INT_MAX) return FA_ERR_BAD_SHAPE;
+    if (static_cast<int64_t>(B) * Hq * Sq > INT_MAX) return FA_ERR_BAD_SHAPE;  // merge: a workgroup per row at most
     const int64_t need = split_workspace_bytes(B, Hq, Sq, d_v, n_split);
     if (need < 0 || workspace == nullptr || static_cast<uint64_t>(need) > workspace_bytes) return FA_ERR_WORKSPACE;
     if (!aligned(workspace, 16)) return FA_ERR_UNSUPPORTED;
@@ -169,7 +170,7 @@ fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, 
   if (static_cast<int64_t>(Sq) * dmax > INT_MAX || static_cast<int64_t>(Sk) * dmax > INT_MAX) return FA_ERR_BAD_SHAPE;
   if (!q_rows) return FA_OK;
   const int64_t n_cb = (static_cast<int64_t>(Hq / Hkv) * Sq + 31) / 32;
-  if (static_cast<int64_t>(B) * Hkv * n_cb * n_parts > INT_MAX || static_cast<int64_t>(B) * Hq > INT_MAX)
+  if (static_cast<int64_t>(B) * Hkv * n_cb * n_parts > INT_MAX || static_cast<int64_t>(B) * Hq * Sq > INT_MAX)
     return FA_ERR_BAD_SHAPE;
   const int64_t need = split_workspace_bytes(B, Hq, Sq, d_v, n_parts);
   if (need < 0 || workspace == nullptr || static_cast<uint64_t>(need) > workspace_bytes) return FA_ERR_WORKSPACE;

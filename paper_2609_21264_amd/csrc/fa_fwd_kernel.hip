@@ -715,32 +715,56 @@ hipError_t launch_dims(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t 
 
 // Merge of the n_split partial results of every query row (log-sum-exp combination): with
 // M = max_s LSE_s, w_s = exp(LSE_s - M), O = sum_s w_s O_s / sum_s w_s and LSE = M + ln(sum_s w_s).
-// A row whose parts are all empty (LSE_s = -inf) gets O = 0 and LSE = -inf. One thread per row and
-// 4 output dims; reads fp32, writes bf16 (round to nearest even) and the fp32 LSE.
+// A row whose parts are all empty (LSE_s = -inf) gets O = 0 and LSE = -inf. A row is handled by
+// DV / 4 * pg threads: thread (g, q) takes output dims 4q .. 4q+3 of the parts s = g (mod pg), so the
+// loads of a row are independent and in flight together; the pg partial maxima, weighted sums and
+// weight sums are combined through LDS. pg is the smallest power of two >= n_split, at most
+// 256 / (DV / 4); a workgroup of 256 threads takes 256 / (DV / 4 * pg) rows. Reads fp32, writes bf16
+// (round to nearest even) and the fp32 LSE.
 template <int DV>
-__global__ __launch_bounds__(256) void fa_merge_kernel(MergeParams p) {
-  constexpr int TPR = DV / 4;  // threads per row
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t row = gid / TPR;
-  const int q = (int)(gid % TPR);
-  if (row >= p.rows) return;
+__global__ __launch_bounds__(256) void fa_merge_kernel(MergeParams p, int pg) {
+  constexpr int TD = DV / 4;     // threads per part group (one per 4 output dims)
+  constexpr int NG = 256 / TD;   // part groups per workgroup
+  __shared__ float s_m[NG], s_den[NG];
+  __shared__ f32x4 s_acc[NG][TD];
+  const int q = threadIdx.x % TD, gw = threadIdx.x / TD;  // group within the workgroup
+  const int g = gw % pg;                                  // part group within the row
+  const int64_t row = (int64_t)blockIdx.x * (NG / pg) + gw / pg;
+  const bool live = row < p.rows;
+  const int g0 = gw - g;                                  // first group of this row
   float m = -INFINITY;
-  for (int sp = 0; sp < p.n_split; ++sp) m = fmaxf(m, p.lse_part[sp * p.rows + row]);
+  if (live)
+    for (int sp = g; sp < p.n_split; sp += pg) m = fmaxf(m, p.lse_part[sp * p.rows + row]);
+  if (q == 0) s_m[gw] = m;
+  __syncthreads();
+  float M = -INFINITY;
+  for (int k = 0; k < pg; ++k) M = fmaxf(M, s_m[g0 + k]);
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float den = 0.f;
-  if (m != -INFINITY) {
-    for (int sp = 0; sp < p.n_split; ++sp) {
-      const float w = expf(p.lse_part[sp * p.rows + row] - m);
+  if (live && M != -INFINITY) {
+    for (int sp = g; sp < p.n_split; sp += pg) {
+      const float w = expf(p.lse_part[sp * p.rows + row] - M);
       den += w;
       acc += w * *reinterpret_cast<const f32x4*>(p.o_part + (sp * p.rows + row) * DV + 4 * q);
     }
-    acc *= 1.f / den;
   }
-  f32x2 lo = {acc.x, acc.y}, hi = {acc.z, acc.w};
-  *reinterpret_cast<uint2*>(p.o + row * DV + 4 * q) =
-      make_uint2(bit_cast<uint32_t>(__builtin_convertvector(lo, bf16x2)),
-                 bit_cast<uint32_t>(__builtin_convertvector(hi, bf16x2)));
-  if (q == 0 && p.lse != nullptr) p.lse[row] = m == -INFINITY ? -INFINITY : m + logf(den);
+  s_acc[gw][q] = acc;
+  if (q == 0) s_den[gw] = den;
+  __syncthreads();
+  if (live && g == 0) {
+    float dsum = 0.f;
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < pg; ++k) {
+      dsum += s_den[g0 + k];
+      o += s_acc[g0 + k][q];
+    }
+    o *= dsum > 0.f ? 1.f / dsum : 0.f;
+    f32x2 lo = {o.x, o.y}, hi = {o.z, o.w};
+    *reinterpret_cast<uint2*>(p.o + row * DV + 4 * q) =
+        make_uint2(bit_cast<uint32_t>(__builtin_convertvector(lo, bf16x2)),
+                   bit_cast<uint32_t>(__builtin_convertvector(hi, bf16x2)));
+    if (q == 0 && p.lse != nullptr) p.lse[row] = dsum > 0.f ? M + logf(dsum) : -INFINITY;
+  }
 }
 
 }  // namespace
@@ -758,9 +782,12 @@ hipError_t launch_forward(FwdParams p, int d_qk, int d_v, bool causal, hipStream
 }
 
 hipError_t launch_merge(MergeParams m, int d_v, hipStream_t stream) {
-  const int64_t threads = m.rows * (d_v / 4);
-  const dim3 grid((unsigned)((threads + 255) / 256));
-  void* args[] = {&m};
+  const int groups = 256 / (d_v / 4);
+  int pg = 1;
+  while (pg < m.n_split && pg < groups) pg *= 2;
+  const int64_t rows_per_wg = groups / pg;
+  const dim3 grid((unsigned)((m.rows + rows_per_wg - 1) / rows_per_wg));
+  void* args[] = {&m, &pg};
   const void* k = d_v == 64 ? reinterpret_cast<const void*>(&fa_merge_kernel<64>)
                             : reinterpret_cast<const void*>(&fa_merge_kernel<128>);
   return hipLaunchKernel(k, grid, dim3(256), args, 0, stream);
