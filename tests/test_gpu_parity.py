@@ -9,6 +9,7 @@ import numpy as np
 import pytest
 import torch
 
+import paper_2609_21264_amd as fa
 import workloads as W
 from parity import check_full, check_rows, compare, run_gpu, to_f64
 from oracle import naive_attention
@@ -143,3 +144,23 @@ def test_single_hip_runtime_mapped():
     libs = {ln.split()[-1] for ln in maps if "libamdhip64" in ln}
     assert len(libs) == 1, libs
     assert any("libfa.so" in ln for ln in maps)
+
+
+@pytest.mark.parametrize("n_split", [1, 3], ids=["fused", "split3"])
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_rising_maxima_rebase_at_every_position(causal, n_split):
+    """Keys whose scores jump far above everything before them, in the second key tile, two middle
+    tiles and the last one (scaled by 4, 8, 16 and 32: exact in bf16, scores up to ~±100 in natural
+    units), so that a lane's exponential sum passes the bound and the tile is redone from its exact
+    row maximum at each of those positions; every output row against the oracle."""
+    w = _case("spikes", dqk=128, dv=128, Hq=2, Hkv=1, Sq=640, Sk=640, causal=causal, seed=81)
+    q, k, v = W.make_inputs(w)
+    for key, factor in ((70, 4.0), (300, 8.0), (520, 16.0), (600, 32.0)):
+        k[:, :, key] *= factor
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    o, lse = fa.forward(qd, kd, vd, causal=causal, scale=w.scale, return_lse=True, n_split=n_split)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), to_f64(v), w.scale, causal)
+    # the spikes really dominate some rows: their LSE rises far above ln(Sk)
+    assert np.nanmax(lse_ref) > 20.0
+    compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, f"spikes causal={causal} split={n_split}")
