@@ -339,9 +339,9 @@ fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
     int64_t heads = cap / Sq;
     if (heads > n_bh) heads = n_bh;
     if (heads >= p.group) heads -= heads % p.group;
-    for (int bh0 = 0; bh0 < n_bh; bh0 += static_cast<int>(heads)) {
+    for (int64_t bh0 = 0; bh0 < n_bh; bh0 += heads) {  // 64-bit: bh0 + heads may pass INT_MAX
       const int nbh = static_cast<int>(n_bh - bh0 < heads ? n_bh - bh0 : heads);
-      if (!run(bh0, nbh, 0, n_qb)) return FA_ERR_HIP;
+      if (!run(static_cast<int>(bh0), nbh, 0, n_qb)) return FA_ERR_HIP;
     }
   } else {
     // Part of one head per chunk.
