@@ -22,8 +22,8 @@
 //    softmax arithmetic is spread evenly between the MFMAs and one wave per SIMD keeps the matrix
 //    unit fed while it issues VALU work (VALU work from the same wave overlaps a running MFMA).
 //  * K/V tiles move HBM -> LDS with buffer loads that write LDS directly (no VGPR staging, no LDS
-//    write instructions), in two rings: K tiles (3 slots, step j loads K(j+3)) and V tiles (4
-//    slots, step j loads V(j+2)). One wait on the wave's own loads plus one barrier per step
+//    write instructions), in two rings: K tiles (2 slots by default, step j loads K(j+2)) and V
+//    tiles (4 slots, step j loads V(j+2)). One wait on the wave's own loads plus one barrier per step
 //    publishes the tiles of the step and frees the slots of the previous one. Rows past Sk load as
 //    zeros (buffer range check), so partial tiles need no special path.
 //  * 16-byte LDS chunks are XOR-swizzled per row (K: by the reading lane's key slot; V: by the key
@@ -51,6 +51,14 @@ namespace {
 #endif
 #ifndef FA_VPF
 #define FA_VPF 6
+#endif
+// K and V ring slots (tiles resident in LDS per workgroup). Loading K only two tiles ahead measured
+// 2-3 % faster than three on the 8K, 4K-d192 and 128K prefill shapes (one box, interleaved).
+#ifndef FA_NKR
+#define FA_NKR 2
+#endif
+#ifndef FA_NVR
+#define FA_NVR 4
 #endif
 
 constexpr float kLn2 = 0.69314718055994530942f;
@@ -110,7 +118,10 @@ struct Cfg {
   static constexpr int VCH = DV / 8;           // 16-byte chunks per V-tile row
   static constexpr int K_BYTES = BN * DQK * 2;
   static constexpr int V_BYTES = BN * DV * 2;
-  static constexpr int NKR = 3, NVR = 4;       // K and V ring slots
+  // Ring slots. Step j loads K(j + KA) into the slot of K(j) and V(j + VA) into the slot of V(j-2):
+  // both were last read in step j-1, which every wave has finished at the barrier of step j.
+  static constexpr int NKR = FA_NKR, NVR = FA_NVR;
+  static constexpr int KA = NKR, VA = NVR - 2;  // how far ahead step j loads K and V tiles
   static constexpr int LDS_BYTES = NKR * K_BYTES + NVR * V_BYTES;
   // Direct-to-LDS loads per wave per tile (each moves 64 lanes x 16 bytes).
   static constexpr int K_LOADS = BN * KCH / 64 / NWAVES;
@@ -118,7 +129,10 @@ struct Cfg {
   static_assert(DQK % 32 == 0 && DV % 64 == 0, "head dims: d_qk multiple of 32, d_v multiple of 64");
   static_assert(BN == 64, "the step schedule assumes 64-key tiles (4 chunks of 16 keys)");
   static_assert((BN * KCH) % (64 * NWAVES) == 0 && (BN * VCH) % (64 * NWAVES) == 0, "tile split over waves");
-  static_assert(2 * V_LOADS + K_LOADS < 64, "vmcnt range");
+  // KA - 1 <= VA <= KA: V(j-1) is issued before K(j+1) (so one counted wait covers both), and the
+  // prologue's groups j = -KA .. -1 hold every tile's first load.
+  static_assert(NKR >= 2 && NKR + 1 <= NVR && NVR <= NKR + 2, "ring sizes");
+  static_assert(KA * (K_LOADS + V_LOADS) < 64 && VA * (K_LOADS + V_LOADS) < 64, "vmcnt range");
   static_assert(LDS_BYTES <= 163840, "LDS budget");
 };
 
@@ -466,23 +480,25 @@ void fa_fwd_kernel(FwdParams p) {
     for (int ks = 0; ks < A::KS; ++ks) load_q(st.qf[qb][ks], qh + (size_t)row * DQK + ks * 16 + st.h * 8);
   }
 
-  // Rings: step j loads K(j+3) and V(j+2) (the group of step j); the prologue loads the groups of
-  // j = -3, -2, -1, i.e. K0, K1, V0, K2, V1 in this order. Every group is issued in full: a tile at
-  // or past the last one loads zeros into a slot nobody reads any more, so the number of loads
-  // issued after any given one is a constant and every wait below is a fixed count.
+  // Rings: step j loads K(j+KA) and V(j+VA) (the group of step j); the prologue loads the groups of
+  // j = -KA .. -1 (with the defaults KA = VA = 2: K0, V0, K1, V1 in this order), each group's V tile
+  // only from V0 on. Every group is issued in full: a tile at or past the last one loads
+  // zeros into a slot nobody reads any more, so the number of loads issued after any given one is a
+  // constant and every wait below is a fixed count.
   TileLoader<C::NWAVES, BN, C::KCH> kload;
   TileLoader<C::NWAVES, BN, C::VCH> vload;
   kload.init(kh, kv_lim, wave, lane, kswz);
   vload.init(vh, kv_lim, wave, lane, vswz);
   auto kslot = [&](int t) { return smem + (t % C::NKR) * C::K_BYTES; };
   auto vslot = [&](int t) { return smem + C::NKR * C::K_BYTES + (t % C::NVR) * C::V_BYTES; };
-  kload.issue(kb0, kslot(0), wave);
-  kload.issue(kb0 + BN, kslot(1), wave);
-  vload.issue(kb0, vslot(0), wave);
-  kload.issue(kb0 + 2 * BN, kslot(2), wave);
-  vload.issue(kb0 + BN, vslot(1), wave);
-  // Q and K0 must have landed: K1, V0, K2, V1 were issued after K0.
-  wait_vmcnt<2 * C::K_LOADS + 2 * C::V_LOADS>();
+#pragma unroll
+  for (int g = -C::KA; g < 0; ++g) {
+    kload.issue(kb0 + (g + C::KA) * BN, kslot(g + C::KA), wave);
+    if (g + C::VA >= 0) vload.issue(kb0 + (g + C::VA) * BN, vslot(g + C::VA), wave);
+  }
+  // Q and K0 must have landed: issued after K0 are V0 when VA = KA, then the groups of j = -KA+1 ..
+  // -1 (K and V each, since VA >= KA - 1).
+  wait_vmcnt<(C::VA == C::KA ? C::V_LOADS : 0) + (C::KA - 1) * (C::K_LOADS + C::V_LOADS)>();
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -519,20 +535,22 @@ void fa_fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int r = 0; r < 8; ++r) pB[kb][qb][r] = 0u;
   }
-  // Before step j: K(j+1) and V(j-1) must have landed; this wave's loads issued after K(j+1) are
-  // V(j), K(j+2) and V(j+1). The barrier then publishes every wave's part and guarantees that all
-  // waves are done with step j-1, whose slots (K(j), V(j-2)) the loads of step j overwrite.
+  // Before step j: K(j+1) and V(j-1) must have landed. K(j+1) belongs to the group of step j+1-KA;
+  // this wave's loads issued after it are that group's V tile and the KA-2 groups after it (with
+  // the defaults only V(j+1)); V(j-1), from the group of step j+1-NVR, came before it.
+  // The barrier then publishes every wave's part and guarantees that all waves are done with step
+  // j-1, whose slots (K(j), V(j-2)) the loads of step j overwrite.
   u32x4 gk = {}, gv = {};
   uint32_t gkl = 0, gvl = 0;
   auto sync_step = [&](int j) {
-    wait_vmcnt<2 * C::V_LOADS + C::K_LOADS>();
+    wait_vmcnt<C::V_LOADS + (C::KA - 2) * (C::K_LOADS + C::V_LOADS)>();
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    gk = kload.rsrc(kb0 + (j + 3) * BN);
-    gkl = kload.lds(kslot(j + 3), wave);
-    gv = vload.rsrc(kb0 + (j + 2) * BN);
-    gvl = vload.lds(vslot(j + 2), wave);
+    gk = kload.rsrc(kb0 + (j + C::KA) * BN);
+    gkl = kload.lds(kslot(j + C::KA), wave);
+    gv = vload.rsrc(kb0 + (j + C::VA) * BN);
+    gvl = vload.lds(vslot(j + C::VA), wave);
   };
   auto issue = [&](int k) {
     if (k < C::K_LOADS)
@@ -559,8 +577,8 @@ void fa_fwd_kernel(FwdParams p) {
     // registers and the copies that merge them could read MFMA results before they are written.
     // (The select is a bit mask: a ternary on the elements would be folded into a select of the
     // two arrays' addresses, which forces both into scratch memory.) V(nt-1) belongs to the load
-    // group of step nt-3; the groups of steps nt-2 and nt-1 may still be in flight.
-    wait_vmcnt<2 * (C::K_LOADS + C::V_LOADS)>();
+    // group of step nt-1-VA; the VA groups after it may still be in flight.
+    wait_vmcnt<C::VA * (C::K_LOADS + C::V_LOADS)>();
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
