@@ -403,7 +403,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the fused attention kernel runs on a "
-              "single MI355X and this build has no multi-GPU path.", file=sys.stderr)
+              "single MI355X and the library has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
     import torch
