@@ -58,7 +58,7 @@ def traffic_from_profile(config: int):
         return None
     fields = {}
     for line in open(path):
-        m = re.match(r"^\s*([a-z_]+)\s*[:=]\s*([0-9a-fA-Fx.eE+-]+)\s*$", line)
+        m = re.match(r"^\s*([a-z0-9_]+)\s*[:=]\s*([0-9a-fA-Fx.eE+-]+)\s*$", line)
         if m:
             fields[m.group(1)] = m.group(2)
     if fields.get("kernel_source_sha256_16") != kernel_source_hash():
