@@ -27,8 +27,8 @@
  * state beyond its compiled kernels, and is reentrant and thread-safe. Q, K, V are only read; O and
  * LSE are only written, every element exactly once per call.
  *
- * Asynchrony: the work is enqueued on `stream` (a hipStream_t passed as void*; NULL is the null
- * stream of the current device); FA_OK means "enqueued". The library never synchronises. Faults
+ * Asynchrony: the work is enqueued on `stream` (NULL is the null stream of the current device);
+ * FA_OK means "enqueued". The library never synchronises. Faults
  * during execution surface at the caller's next synchronisation.
  *
  * Errors: every argument check runs on the host before any HIP call. On any error return nothing is
@@ -47,6 +47,10 @@
 #define FA_MI355X_FA_H
 
 #include <stddef.h>
+
+/* HIP's stream handle, the same declaration as in hip/hip_runtime_api.h, so that this header needs
+ * no HIP include (C callers may include either header first). */
+typedef struct ihipStream_t* hipStream_t;
 
 #ifdef __cplusplus
 extern "C" {
@@ -71,7 +75,7 @@ typedef enum {
  * Same contract as fa_fwd_ex(Q, K, V, O, NULL, B, Hq, Hkv, Sq, Sk, d, d, scale, causal, stream).
  */
 fa_status_t fa_fwd(const void* Q, const void* K, const void* V, void* O, int B, int Hq, int Hkv,
-                   int Sq, int Sk, int d, float scale, int causal, void* stream);
+                   int Sq, int Sk, int d, float scale, int causal, hipStream_t stream);
 
 /*
  * fa_fwd_ex -- general entry point.
@@ -83,11 +87,11 @@ fa_status_t fa_fwd(const void* Q, const void* K, const void* V, void* O, int B, 
  *   scale     multiplier of the scores (the paper uses 1/sqrt(d_k)); any finite value, including
  *             0 (uniform weights over the visible keys) and negative values
  *   causal    nonzero for bottom-right causal masking
- *   stream    hipStream_t to enqueue on
+ *   stream    the HIP stream to enqueue on
  */
 fa_status_t fa_fwd_ex(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
                       int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
-                      void* stream);
+                      hipStream_t stream);
 
 /*
  * fa_fwd_split -- the same operation with every query block's key range cut into n_split parts that
@@ -116,7 +120,7 @@ fa_status_t fa_fwd_ex(const void* Q, const void* K, const void* V, void* O, floa
  */
 fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
                          int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
-                         int n_split, void* workspace, size_t workspace_bytes, void* stream);
+                         int n_split, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Workspace bytes fa_fwd_split needs: n_split * B * Hq * Sq * (d_v + 1) * 4; 0 when B, Hq, Sq, d_v
  * or n_split is <= 0 (nothing to store); SIZE_MAX if the count overflows. */
@@ -151,7 +155,7 @@ size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split)
  */
 fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
                           int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
-                          int n_parts, void* workspace, size_t workspace_bytes, void* stream);
+                          int n_parts, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Suggested n_parts for fa_fwd_decode on a device with n_cu compute units: about one workgroup per
  * CU in total, no part shorter than 4 key tiles (512 keys), at least 1. Host arithmetic only.
@@ -201,11 +205,11 @@ int fa_fwd_split_parts(int n_cu, int B, int Hq, int Sq, int Sk, int d_qk, int d_
  * FA_OK without a launch. Each operator enqueues one kernel on `stream`.
  */
 fa_status_t fa_lbl_scores(const void* Q, const void* K, void* S, int B, int Hq, int Hkv, int Sq, int Sk,
-                          int d_qk, float scale, int causal, void* stream);
+                          int d_qk, float scale, int causal, hipStream_t stream);
 fa_status_t fa_lbl_softmax(const void* S, void* P, float* LSE, int B, int Hq, int Sq, int Sk, int causal,
-                           void* stream);
+                           hipStream_t stream);
 fa_status_t fa_lbl_pv(const void* P, const void* V, void* O, int B, int Hq, int Hkv, int Sq, int Sk, int d_v,
-                      int causal, void* stream);
+                      int causal, hipStream_t stream);
 
 /* Row stride ld (elements) of the spill buffers: Sk rounded up to 64; -1 if Sk < 0 or Sk > 2^22. */
 int fa_lbl_ld(int Sk);
@@ -232,7 +236,7 @@ size_t fa_lbl_workspace_bytes(int B, int Hq, int Sq, int Sk);
  */
 fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq,
                            int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
-                           void* workspace, size_t workspace_bytes, void* stream);
+                           void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Static, human-readable name of a status code ("FA_OK", ...); "unknown status" otherwise. */
 const char* fa_status_str(fa_status_t s);

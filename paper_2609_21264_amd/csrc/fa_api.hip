@@ -26,7 +26,7 @@ int64_t split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split) {
 }
 
 fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
-                    int Sq, int Sk, int d_qk, int d_v, float scale, int causal, void* stream, int n_split = 0,
+                    int Sq, int Sk, int d_qk, int d_v, float scale, int causal, hipStream_t stream, int n_split = 0,
                     void* workspace = nullptr, size_t workspace_bytes = 0) {
   if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0) return FA_ERR_BAD_SHAPE;
   if (Hq > 0 && (Hkv <= 0 || Hq % Hkv != 0)) return FA_ERR_BAD_SHAPE;
@@ -78,9 +78,9 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
     p.n_split = n_split;
     p.o_part = static_cast<float*>(workspace);
     p.lse_part = p.o_part + rows * n_split * d_v;
-    err = fa::launch_forward_split(p, d_qk, d_v, causal != 0, static_cast<hipStream_t>(stream));
+    err = fa::launch_forward_split(p, d_qk, d_v, causal != 0, stream);
   } else {
-    err = fa::launch_forward(p, d_qk, d_v, causal != 0, static_cast<hipStream_t>(stream));
+    err = fa::launch_forward(p, d_qk, d_v, causal != 0, stream);
   }
   return err == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
@@ -133,18 +133,18 @@ fa::LblParams lbl_params(int B, int Hq, int Hkv, int Sq, int Sk, float scale, in
 extern "C" {
 
 fa_status_t fa_fwd_ex(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
-                      int Sq, int Sk, int d_qk, int d_v, float scale, int causal, void* stream) {
+                      int Sq, int Sk, int d_qk, int d_v, float scale, int causal, hipStream_t stream) {
   return forward(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, scale, causal, stream);
 }
 
 fa_status_t fa_fwd(const void* Q, const void* K, const void* V, void* O, int B, int Hq, int Hkv, int Sq, int Sk,
-                   int d, float scale, int causal, void* stream) {
+                   int d, float scale, int causal, hipStream_t stream) {
   return forward(Q, K, V, O, nullptr, B, Hq, Hkv, Sq, Sk, d, d, scale, causal, stream);
 }
 
 fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
                          int Sq, int Sk, int d_qk, int d_v, float scale, int causal, int n_split, void* workspace,
-                         size_t workspace_bytes, void* stream) {
+                         size_t workspace_bytes, hipStream_t stream) {
   if (n_split < 1) return FA_ERR_BAD_SHAPE;
   return forward(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, scale, causal, stream, n_split, workspace,
                  workspace_bytes);
@@ -152,7 +152,7 @@ fa_status_t fa_fwd_split(const void* Q, const void* K, const void* V, void* O, f
 
 fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
                           int Sq, int Sk, int d_qk, int d_v, float scale, int causal, int n_parts, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+                          size_t workspace_bytes, hipStream_t stream) {
   if (n_parts < 1) return FA_ERR_BAD_SHAPE;
   if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0) return FA_ERR_BAD_SHAPE;
   if (Hq > 0 && (Hkv <= 0 || Hq % Hkv != 0)) return FA_ERR_BAD_SHAPE;
@@ -196,7 +196,7 @@ fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, 
   const int64_t rows = static_cast<int64_t>(B) * Hq * Sq;
   p.o_part = static_cast<float*>(workspace);
   p.lse_part = p.o_part + rows * n_parts * d_v;
-  return fa::launch_decode(p, d_qk, d_v, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+  return fa::launch_decode(p, d_qk, d_v, stream) == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
 
 int fa_fwd_decode_parts(int n_cu, int B, int Hq, int Hkv, int Sq, int Sk) {
@@ -243,7 +243,7 @@ size_t fa_lbl_workspace_bytes(int B, int Hq, int Sq, int Sk) {
 }
 
 fa_status_t fa_lbl_scores(const void* Q, const void* K, void* S, int B, int Hq, int Hkv, int Sq, int Sk, int d_qk,
-                          float scale, int causal, void* stream) {
+                          float scale, int causal, hipStream_t stream) {
   fa_status_t st = lbl_check_shape(B, Hq, Hkv, Sq, Sk, d_qk, 0);
   if (st != FA_OK) return st;
   const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
@@ -257,11 +257,11 @@ fa_status_t fa_lbl_scores(const void* Q, const void* K, void* S, int B, int Hq, 
   p.q = static_cast<const uint16_t*>(Q);
   p.k = static_cast<const uint16_t*>(K);
   p.s = static_cast<uint16_t*>(S);
-  return fa::launch_lbl_scores(p, d_qk, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+  return fa::launch_lbl_scores(p, d_qk, stream) == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
 
 fa_status_t fa_lbl_softmax(const void* S, void* P, float* LSE, int B, int Hq, int Sq, int Sk, int causal,
-                           void* stream) {
+                           hipStream_t stream) {
   fa_status_t st = lbl_check_shape(B, Hq, Hq > 0 ? 1 : 0, Sq, Sk, 0, 0);
   if (st != FA_OK) return st;
   const bool rows = static_cast<int64_t>(B) * Hq * Sq > 0;
@@ -272,11 +272,11 @@ fa_status_t fa_lbl_softmax(const void* S, void* P, float* LSE, int B, int Hq, in
   p.s = const_cast<uint16_t*>(static_cast<const uint16_t*>(S));
   p.p = static_cast<uint16_t*>(P);
   p.lse = LSE;
-  return fa::launch_lbl_softmax(p, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+  return fa::launch_lbl_softmax(p, stream) == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
 
 fa_status_t fa_lbl_pv(const void* P, const void* V, void* O, int B, int Hq, int Hkv, int Sq, int Sk, int d_v,
-                      int causal, void* stream) {
+                      int causal, hipStream_t stream) {
   fa_status_t st = lbl_check_shape(B, Hq, Hkv, Sq, Sk, 0, d_v);
   if (st != FA_OK) return st;
   const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
@@ -289,12 +289,12 @@ fa_status_t fa_lbl_pv(const void* P, const void* V, void* O, int B, int Hq, int 
   p.p = const_cast<uint16_t*>(static_cast<const uint16_t*>(P));
   p.v = static_cast<const uint16_t*>(V);
   p.o = static_cast<uint16_t*>(O);
-  return fa::launch_lbl_pv(p, d_v, static_cast<hipStream_t>(stream)) == hipSuccess ? FA_OK : FA_ERR_HIP;
+  return fa::launch_lbl_pv(p, d_v, stream) == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
 
 fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
                            int Sq, int Sk, int d_qk, int d_v, float scale, int causal, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+                           size_t workspace_bytes, hipStream_t stream) {
   fa_status_t st = lbl_check_shape(B, Hq, Hkv, Sq, Sk, d_qk, d_v);
   if (st != FA_OK) return st;
   const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
@@ -321,7 +321,7 @@ fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
   p.lse = LSE;
   p.s = p.p = static_cast<uint16_t*>(workspace);  // probabilities overwrite the scores in place
   const int n_bh = B * Hq, n_qb = p.nqb;
-  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipStream_t s = stream;
   auto run = [&](int bh0, int nbh, int qb0, int nqb) {
     p.bh0 = bh0;
     p.nbh = nbh;

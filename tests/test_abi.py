@@ -3,6 +3,8 @@ every invalid argument on the host before any HIP call (so nothing is launched).
 
 import ctypes
 import os
+import shutil
+import subprocess
 import re
 
 import pytest
@@ -350,3 +352,32 @@ def test_decode_parts_heuristic(lib):
     for args in ((0, 1, 32, 8, 1, 100), (256, 0, 32, 8, 1, 100), (256, 1, 32, 5, 1, 100), (256, 1, 32, 8, 0, 100),
                  (256, 1, 32, 8, 1, -1)):
         assert fa.fa_fwd_decode_parts(*args) == 0
+
+
+def _compile(cmd, source, suffix, tmp_path):
+    path = tmp_path / f"t{suffix}"
+    path.write_text(source)
+    res = subprocess.run(cmd + [str(path)], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+
+
+def test_header_compiles_as_c99(tmp_path):
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = '#include "fa.h"\nint main(void) { hipStream_t s = NULL; return (int)fa_fwd(0, 0, 0, 0, 0, 0, 0, 0, 0, 64, 1.0f, 0, s); }\n'
+    _compile(["gcc", "-x", "c", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-I", os.path.dirname(HEADER)],
+             src, ".c", tmp_path)
+
+
+@pytest.mark.parametrize("hip_first", [True, False], ids=["hip-header-first", "fa-header-first"])
+def test_header_stream_type_is_hips(tmp_path, hip_first):
+    """fa.h declares hipStream_t exactly as HIP does, so either header may come first."""
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    inc = ['#include <hip/hip_runtime_api.h>', '#include "fa.h"']
+    if not hip_first:
+        inc.reverse()
+    src = "\n".join(inc) + "\nint main() { hipStream_t s = nullptr; hipStreamCreate(&s); return (int)fa_fwd(0, 0, 0, 0, 0, 0, 0, 0, 0, 64, 1.f, 0, s); }\n"
+    _compile([hipcc, "-fsyntax-only", "-Wno-unused-command-line-argument", "-I", os.path.dirname(HEADER)],
+             src, ".cpp", tmp_path)
