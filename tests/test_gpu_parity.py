@@ -164,3 +164,44 @@ def test_rising_maxima_rebase_at_every_position(causal, n_split):
     # the spikes really dominate some rows: their LSE rises far above ln(Sk)
     assert np.nanmax(lse_ref) > 20.0
     compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, f"spikes causal={causal} split={n_split}")
+
+
+def test_concurrent_threads_and_streams():
+    """The library keeps no state: two host threads, each on its own stream with its own problem,
+    calling the fused and split entry points concurrently, get exactly the single-stream results."""
+    import threading
+
+    cases = [_case("t0", dqk=128, dv=128, Hq=4, Hkv=2, Sq=333, Sk=517, causal=True, seed=91),
+             _case("t1", dqk=64, dv=64, Hq=3, Hkv=1, Sq=200, Sk=700, causal=False, seed=92)]
+    data = []
+    for w in cases:
+        q, k, v = (t.cuda() for t in W.make_inputs(w))
+        ref = [fa.forward(q, k, v, causal=w.causal, scale=w.scale, return_lse=True, n_split=ns) for ns in (1, 3)]
+        torch.cuda.synchronize()
+        data.append((w, q, k, v, [(o.clone(), l.clone()) for o, l in ref]))
+    errors = []
+
+    def worker(idx):
+        w, q, k, v, ref = data[idx]
+        stream = torch.cuda.Stream()
+        try:
+            with torch.cuda.stream(stream):
+                outs = []
+                for rep in range(20):
+                    ns = (1, 3)[rep % 2]
+                    outs.append((ns, fa.forward(q, k, v, causal=w.causal, scale=w.scale, return_lse=True,
+                                                n_split=ns, stream=stream)))
+            stream.synchronize()
+            for ns, (o, l) in outs:
+                ro, rl = ref[0 if ns == 1 else 1]
+                if not (torch.equal(o, ro) and torch.equal(l, rl)):
+                    errors.append(f"{w.name} n_split={ns}")
+        except Exception as e:  # reported in the main thread
+            errors.append(f"{w.name}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(data))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
