@@ -120,7 +120,7 @@ def test_check_order(lib):
     assert call(scale=float("nan"), Q=QP + 2) == fa.FA_ERR_BAD_SCALE
 
 
-def test_north_star_entry_point_validates(lib):
+def test_fa_fwd_entry_point_validates_on_host(lib):
     L = lib
     assert L.fa_fwd(QP, KP, VP, OP, 1, 4, 2, 64, 64, 100, 0.1, 0, None) == fa.FA_ERR_UNSUPPORTED
     assert L.fa_fwd(QP, KP, VP, None, 1, 4, 2, 64, 64, 64, 0.1, 0, None) == fa.FA_ERR_NULL_POINTER

@@ -205,3 +205,23 @@ def test_concurrent_threads_and_streams():
     for t in threads:
         t.join()
     assert not errors, errors
+
+
+def test_fa_fwd_entry_point():
+    """fa_fwd (one head dimension, no LSE) through the C ABI: the oracle's result, and bit for bit the
+    output of fa_fwd_ex on the same inputs."""
+    w = _case("fa_fwd d128 gqa causal", dqk=128, dv=128, B=2, Hq=8, Hkv=2, Sq=300, Sk=420, causal=True, seed=95)
+    q, k, v = W.make_inputs(w)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    o1 = torch.empty(w.B, w.Hq, w.Sq, w.dv, dtype=torch.bfloat16, device="cuda")
+    o2 = torch.empty_like(o1)
+    lse = torch.empty(w.B, w.Hq, w.Sq, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    assert fa.fa_fwd(qd.data_ptr(), kd.data_ptr(), vd.data_ptr(), o1.data_ptr(), w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.dqk,
+                     w.scale, w.causal, stream) == fa.FA_OK
+    assert fa.fa_fwd_ex(qd.data_ptr(), kd.data_ptr(), vd.data_ptr(), o2.data_ptr(), lse.data_ptr(), w.B, w.Hq, w.Hkv,
+                        w.Sq, w.Sk, w.dqk, w.dv, w.scale, w.causal, stream) == fa.FA_OK
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+    o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), to_f64(v), w.scale, w.causal)
+    compare(to_f64(o1), lse.cpu().double().numpy(), o_ref, lse_ref, w.name)
