@@ -382,6 +382,9 @@ def main():
     ap.add_argument("--workload", default=None,
                     help="a named further workload instead of --config (split-mode shapes: "
                          "decode-128k, decode16-128k-causal, decode-b8-8k)")
+    ap.add_argument("--shape", default=None, metavar="B,Hq,Hkv,Sq,Sk,d_qk,d_v,causal",
+                    help="any other problem instead of --config, e.g. 1,32,8,16384,16384,128,128,1 (seeded "
+                         "N(0,1) inputs, scale 1/sqrt(d_qk))")
     ap.add_argument("--paper-sweep", action="store_true",
                     help="time the paper's own shapes (Table 5 GPT-2 Small sweep and the 12 Table 6 models) "
                          "and print one JSON line with a row per shape, in both FLOP conventions")
@@ -414,7 +417,13 @@ def main():
     import paper_2609_21264_amd as fa
     import workloads as W
 
-    w = W.EXTRA[args.workload] if args.workload else W.CONFIGS[args.config]
+    if args.shape:
+        B, Hq, Hkv, Sq, Sk, dqk, dv, causal = (int(x) for x in args.shape.split(","))
+        w = W.small(f"B{B} Hq{Hq} Hkv{Hkv} Sq{Sq} Sk{Sk} dqk{dqk} dv{dv}" + (" causal" if causal else ""), B=B, Hq=Hq,
+                    Hkv=Hkv, Sq=Sq, Sk=Sk, dqk=dqk, dv=dv, causal=bool(causal), seed=5000)
+        args.workload = w.name  # no committed counter summary for it: traffic stays null
+    else:
+        w = W.EXTRA[args.workload] if args.workload else W.CONFIGS[args.config]
     if args.unfused:
         unfused_main(args, w)
         return
