@@ -15,9 +15,16 @@ JSON line:
 * cpu_baseline -- the fp64 oracle timed on this host on a bounded sample of the same workload
 * parity     -- a few seeded rows per head compared with the oracle (outside the timed region)
 
-Default workload: the Llama-style GQA prefill, B1 Hq32 Hkv8 S8192 d128 causal (config 3). Split mode:
-``--split N|auto`` with ``--workload decode-128k`` (and the other named decode shapes); ``--decode``
-runs the decode-shaped path (query heads of a group packed into 32-column blocks) on those shapes.
+Default workload: the long-context GQA prefill, B1 Hq32 Hkv8 S131072 d128 causal (config 5, the
+largest of the five configurations); ``--config N`` selects another. Split mode: ``--split N|auto``
+with ``--workload decode-128k`` (and the other named decode shapes); ``--decode`` runs the
+decode-shaped path (query heads of a group packed into 32-column blocks) on those shapes.
+
+``--cold`` writes a 512 MiB buffer before every timed launch (outside the events around it), so each
+launch starts with the 4 MB L2s and the 256 MB Infinity Cache holding none of its inputs; ``--ramp N``
+prints the event time of each of N back-to-back launches from the first one on (clock and cache
+warm-up). ``--ceilings`` runs the measured-ceiling microbenchmarks instead
+(``paper_2609_21264_amd/ceilings.py``).
 
 ``--unfused`` times the layer-by-layer baseline (scores, mask + softmax, P V with S and P spilled to
 HBM in bf16) on the same workload instead and prints one JSON line with each operator's HBM roofline
@@ -72,41 +79,70 @@ def traffic_from_profile(config: int):
         return None
 
 
-def cpu_baseline(w, q, k, v, budget_s: float):
-    """Time the fp64 oracle on whole query heads (all rows) until ``budget_s`` has elapsed."""
+def blas_threads() -> int:
+    """Threads NumPy's BLAS runs with (threadpoolctl when present, else OMP_NUM_THREADS, else 1)."""
     import numpy as np
 
+    try:
+        import threadpoolctl
+
+        (np.ones((4, 4)) @ np.ones((4, 4)))  # loads the BLAS so that threadpoolctl sees it
+        info = threadpoolctl.threadpool_info()
+        if info:
+            return max(i["num_threads"] for i in info)
+    except Exception:
+        pass
+    try:
+        return int(os.environ.get("OMP_NUM_THREADS", "1"))
+    except ValueError:
+        return 1
+
+
+def cpu_baseline(w, q, k, v, budget_s: float):
+    """Time the fp64 oracle on this host on a bounded sample of workload ``w``.
+
+    Problems of at most 2^27 score elements per head are timed on whole heads (every query row);
+    larger ones on the seeded 64-row subset of every head that the parity tests use (plus rows 0
+    and Sq-1). Key/value groups (one K/V head and its query heads) are timed one after another until
+    ``budget_s`` has elapsed. The oracle's time grows linearly with the rows it computes (each row
+    is a full row of scores), so the time of the whole problem is the measured time scaled by
+    (B*Hq*Sq) / rows timed; the value is the workload's metric FLOPs over that time.
+    """
+    import numpy as np
+
+    import workloads as W
     from oracle import bf16_bits_to_f64, naive_attention_rows
 
     def f64(t):
         return bf16_bits_to_f64(t.contiguous().view(__import__("torch").int16).numpy())
 
-    threads = os.cpu_count()
-    try:
-        import threadpoolctl
-        (np.ones((4, 4)) @ np.ones((4, 4)))
-        info = threadpoolctl.threadpool_info()
-        if info:
-            threads = max(i["num_threads"] for i in info)
-    except Exception:
-        pass
-    rows_all = np.arange(w.Sq)
-    done_heads, t_oracle = 0, 0.0
-    for idx in range(w.B * w.Hq):
-        b, h = divmod(idx, w.Hq)
-        t0 = time.perf_counter()
-        naive_attention_rows(lambda bb, hh, r: f64(q[bb, hh]), lambda bb, g: f64(k[bb, g]),
-                             lambda bb, g: f64(v[bb, g]), 1, 1, 1, w.Sq, w.scale, w.causal, [rows_all])
-        t_oracle += time.perf_counter() - t0
-        done_heads += 1
+    whole = w.Sq * w.Sk <= (1 << 27)
+    rows = [np.arange(w.Sq)] * (w.B * w.Hq) if whole else W.sample_rows(w, n=64)
+    G = w.group
+    t_oracle, n_heads, n_rows = 0.0, 0, 0
+    for b in range(w.B):
+        for g in range(w.Hkv):
+            rs = [rows[b * w.Hq + g * G + m] for m in range(G)]
+            t0 = time.perf_counter()
+            naive_attention_rows(lambda bb, hh, r: f64(q[b, g * G + hh][r]), lambda bb, gg: f64(k[b, g]),
+                                 lambda bb, gg: f64(v[b, g]), 1, G, 1, w.Sq, w.scale, w.causal, rs)
+            t_oracle += time.perf_counter() - t0
+            n_heads += G
+            n_rows += sum(len(r) for r in rs)
+            if t_oracle >= budget_s:
+                break
         if t_oracle >= budget_s:
             break
-    frac = done_heads / (w.B * w.Hq)
-    import workloads as W
-    tflops = W.metric_flops(w) * frac / t_oracle / 1e12
-    return {"value": tflops, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done_heads} of {w.B * w.Hq} query heads, all {w.Sq} rows each "
-                      f"({t_oracle:.1f} s of fp64 NumPy; metric FLOPs of the sample)"}
+    total_rows = w.B * w.Hq * w.Sq
+    t_full = t_oracle * total_rows / n_rows
+    tflops = W.metric_flops(w) / t_full / 1e12
+    what = "every row" if whole else f"{n_rows // n_heads}-row seeded subsets (64 rows + rows 0 and Sq-1)"
+    return {"value": tflops, "unit": "TFLOP/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{n_heads} of {w.B * w.Hq} query heads, {what}: {n_rows} rows in {t_oracle:.1f} s of fp64 "
+                      f"NumPy, scaled x{total_rows / n_rows:.1f} to the whole problem ({t_full:.0f} s); metric FLOPs",
+            "measured_s": round(t_oracle, 4), "rows_timed": n_rows, "extrapolated_s": round(t_full, 3),
+            "host_cpu_count": os.cpu_count(),
+            "host_cpus_usable": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
 
 
 def parity_sample(w, q, k, v, o, lse, rows_per_head: int = 4):
@@ -122,18 +158,22 @@ def parity_sample(w, q, k, v, o, lse, rows_per_head: int = 4):
     res = naive_attention_rows(lambda b, h, r: f64(q[b, h][r]), lambda b, g: f64(k[b, g]),
                                lambda b, g: f64(v[b, g]), w.B, w.Hq, w.Hkv, w.Sq, w.scale, w.causal, rows)
     oc, lc = o.cpu(), lse.cpu()
-    max_abs, lse_max, n = 0.0, 0.0, 0
+    max_abs, lse_max, n, err_sum, n_el = 0.0, 0.0, 0, 0.0, 0
     for idx, (o_ref, l_ref) in enumerate(res):
         b, h = divmod(idx, w.Hq)
         r = rows[idx]
         og = f64(oc[b, h][r])
-        max_abs = max(max_abs, float(np.abs(og - o_ref).max()))
+        err = np.abs(og - o_ref)
+        max_abs = max(max_abs, float(err.max()) if err.size else 0.0)
+        err_sum += float(err.sum())
+        n_el += err.size
         fin = np.isfinite(l_ref)
         if fin.any():
             lse_max = max(lse_max, float(np.abs(lc[b, h][r].double().numpy()[fin] - l_ref[fin]).max()))
         n += len(r)
-    return {"rows_checked": n, "max_abs": max_abs, "lse_max_abs": lse_max,
-            "pass": bool(max_abs <= 2e-2 and lse_max <= 1e-3)}
+    mean_abs = err_sum / max(n_el, 1)
+    return {"rows_checked": n, "max_abs": max_abs, "mean_abs": mean_abs, "lse_max_abs": lse_max,
+            "pass": bool(max_abs <= 2e-2 and mean_abs <= 2e-3 and lse_max <= 1e-3)}
 
 
 def paper_sweep():
@@ -370,6 +410,38 @@ def unfused_main(args, w):
     print(json.dumps(out), flush=True)
 
 
+def ramp_main(args, w, step, stream):
+    """Event times of ``args.ramp`` back-to-back launches from the very first one (no warmup): how
+    many launches the GPU's clocks and caches take to settle. One JSON line."""
+    import torch
+
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.ramp)]
+    for s, e in ev:
+        s.record(stream)
+        step()
+        e.record(stream)
+    torch.cuda.synchronize()
+    ms = [s.elapsed_time(e) for s, e in ev]
+    n = len(ms)
+    windows = {}
+    for lo, hi in ((0, 1), (1, 10), (10, 50), (50, 100), (100, 200), (200, 400), (400, 800), (800, n)):
+        if lo < n and lo < hi:
+            part = ms[lo:min(hi, n)]
+            windows[f"{lo}-{min(hi, n) - 1}"] = round(sum(part) / len(part), 4)
+    import workloads as W
+
+    flops = W.metric_flops(w)
+    tail = ms[n // 2:]
+    print(json.dumps({"metric": "per-launch kernel time from a cold start (event pairs on the launch stream)",
+                      "unit": "ms", "config": {"workload": w.name}, "launches": n,
+                      "window_mean_ms": windows,
+                      "first_launch_ms": round(ms[0], 4),
+                      "second_half_mean_ms": round(sum(tail) / len(tail), 4),
+                      "second_half_tflops": round(flops / (sum(tail) / len(tail) / 1e3) / 1e12, 1),
+                      "ms": [round(x, 4) for x in ms]}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -378,7 +450,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=-1,
                     help="untimed steps first; default: at least 10 and at least 0.5 s (the first tens of "
                          "milliseconds of back-to-back launches run slower while clocks and caches settle)")
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--workload", default=None,
                     help="a named further workload instead of --config (split-mode shapes: "
                          "decode-128k, decode16-128k-causal, decode-b8-8k)")
@@ -399,18 +471,32 @@ def main():
                     help="largest spill buffer for --unfused (bigger problems run in chunks)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold", action="store_true",
+                    help="write a 512 MiB buffer before each timed launch (outside its events): no input is "
+                         "cache-resident when a launch starts; the value is then computed from the events")
+    ap.add_argument("--ramp", type=int, default=0, metavar="N",
+                    help="instead of the normal run: time N back-to-back launches from the very first one with "
+                         "events and print their times (how long clocks and caches take to settle)")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="run the measured-ceiling microbenchmarks (MFMA rate and clock, HBM streams through VGPR "
+                         "and direct-to-LDS loads, LDS reads) and print one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed steps, run 3 plain device-to-device copies of MIB MiB (a reference "
                          "kernel of known traffic for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
-    if args.paper_sweep:
-        paper_sweep()
-        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the fused attention kernel runs on a "
               "single MI355X and the library has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
+    if args.paper_sweep:
+        paper_sweep()
+        return
+    if args.ceilings:
+        from paper_2609_21264_amd import ceilings
+
+        ceilings.main()
+        return
 
     import torch
 
@@ -429,7 +515,7 @@ def main():
         return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    print(f"[bench] workload {args.config}: {w.name}", file=sys.stderr, flush=True)
+    print(f"[bench] workload: {w.name}", file=sys.stderr, flush=True)
     q_cpu, k_cpu, v_cpu = W.make_inputs(w)
     q, k, v = q_cpu.to(dev), k_cpu.to(dev), v_cpu.to(dev)
     o = torch.empty((w.B, w.Hq, w.Sq, w.dv), dtype=torch.bfloat16, device=dev)
@@ -466,6 +552,14 @@ def main():
         if st != 0:
             raise fa.FaError(st)
 
+    if args.ramp > 0:
+        ramp_main(args, w, step, stream)
+        return
+
+    flush = None
+    if args.cold:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+
     step_s = None  # wall time per step seen during warmup
     if args.warmup >= 0:
         for _ in range(args.warmup):
@@ -494,6 +588,8 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s, e in ev:
+        if flush is not None:
+            flush.fill_(1)  # outside the event pair
         s.record(stream)
         step()
         e.record(stream)
@@ -501,12 +597,18 @@ def main():
     wall = time.perf_counter() - t0
     launch_ms = [s.elapsed_time(e) for s, e in ev]
     print(f"[bench] timed {args.steps} steps in {wall:.4f} s", file=sys.stderr, flush=True)
+    if flush is not None:
+        # the wall clock includes the flushes: the whole-job rate comes from the launches' events
+        wall = sum(launch_ms) / 1e3
+        del flush
 
     flops = W.metric_flops(w)
     value = flops * args.steps / wall / 1e12
     avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
     achieved = flops / avg_launch_s / 1e12
-    traffic = traffic_from_profile(args.config) if not args.workload and not n_split else None
+    traffic = traffic_from_profile(args.config) if not args.workload and not n_split and not args.cold else None
+    kernel_name = ("fa_decode_kernel + fa_merge_kernel" if args.decode else
+                   "fa_fwd_kernel (split) + fa_merge_kernel" if n_split else "fa_fwd_kernel")
     # Bound by operational intensity at HBM (metric FLOPs over algorithmic bytes) against the ridge
     # point of the two peaks.
     nbytes = W.algorithmic_bytes(w)
@@ -553,10 +655,14 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Sq": w.Sq, "Sk": w.Sk,
                    "d_qk": w.dqk, "d_v": w.dv, "causal": w.causal, "scale": w.scale, "seed": w.seed,
-                   "split": n_split or None, "path": "decode" if args.decode else ("split" if n_split else "fused")},
+                   "split": n_split or None, "path": "decode" if args.decode else ("split" if n_split else "fused"),
+                   "caches": "cold (512 MiB written before each launch)" if args.cold else "warm"},
         "roofline": {**roof,
                      "traffic": traffic,
-                     "kernel_ms": {"mean": round(sum(launch_ms) / len(launch_ms), 4), "min": round(min(launch_ms), 4)},
+                     "kernel_ms": {"mean": round(sum(launch_ms) / len(launch_ms), 4),
+                                   "median": round(sorted(launch_ms)[len(launch_ms) // 2], 4),
+                                   "min": round(min(launch_ms), 4), "max": round(max(launch_ms), 4)},
+                     "kernel": kernel_name,
                      "algorithmic_flops_per_launch": flops,
                      "algorithmic_bytes_per_launch": W.algorithmic_bytes(w)},
         "cpu_baseline": cpu,

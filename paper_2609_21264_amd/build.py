@@ -19,6 +19,9 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libfa.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 SOURCES = ["fa_api.hip", "fa_fwd_kernel.hip", "fa_lbl_kernel.hip", "fa_decode_kernel.hip"]
+# Measurement-only microbenchmarks (measured ceilings), a library of their own.
+CEIL_LIB_PATH = os.path.join(PKG_DIR, "libfa_ceilings.so")
+CEIL_SOURCES = ["fa_ceilings.hip"]
 ARCH = "gfx950"
 
 
@@ -45,14 +48,14 @@ def _device_flags() -> list:
     ]
 
 
-def compile_command(out: str, extra=()) -> list:
+def compile_command(out: str, extra=(), sources=SOURCES) -> list:
     return [
         hipcc(), *_device_flags(), "-fPIC", "-shared",
         "-Wall", "-Wno-unused-command-line-argument",
         "-Wl,-rpath,/opt/rocm/lib",
         *extra,
         "-o", out,
-        *[os.path.join(CSRC, s) for s in SOURCES],
+        *[os.path.join(CSRC, s) for s in sources],
     ]
 
 
@@ -66,13 +69,11 @@ def kernel_asm(out: str, source: str = "fa_fwd_kernel.hip") -> None:
         raise RuntimeError("hipcc -S failed:\n" + (res.stdout or "") + (res.stderr or ""))
 
 
-def build(verbose: bool = False, resource_usage: bool = False) -> str:
-    """Compile libfa.so for gfx950 into the package directory; returns its path."""
-    extra = ["-Rpass-analysis=kernel-resource-usage"] if resource_usage else []
-    fd, tmp = tempfile.mkstemp(prefix=".libfa.", suffix=".so.tmp", dir=PKG_DIR)
+def _link(path: str, sources, extra, verbose: bool, show: bool) -> None:
+    fd, tmp = tempfile.mkstemp(prefix="." + os.path.basename(path) + ".", suffix=".so.tmp", dir=PKG_DIR)
     os.close(fd)
     try:
-        cmd = compile_command(tmp, extra)
+        cmd = compile_command(tmp, extra, sources)
         if verbose:
             print(" ".join(cmd), flush=True)
         res = subprocess.run(cmd, capture_output=True, text=True)
@@ -81,12 +82,20 @@ def build(verbose: bool = False, resource_usage: bool = False) -> str:
         lines = [ln for ln in out.splitlines() if "packed-fp32-ops" not in ln or "error" in ln]
         if res.returncode != 0:
             raise RuntimeError("hipcc failed:\n" + "\n".join(lines))
-        if verbose or resource_usage:
+        if verbose or show:
             print("\n".join(lines), flush=True)
-        os.replace(tmp, LIB_PATH)
+        os.replace(tmp, path)
     finally:
         if os.path.exists(tmp):
             os.unlink(tmp)
+
+
+def build(verbose: bool = False, resource_usage: bool = False) -> str:
+    """Compile libfa.so (and the measurement library libfa_ceilings.so) for gfx950 into the package
+    directory; returns the path of libfa.so."""
+    extra = ["-Rpass-analysis=kernel-resource-usage"] if resource_usage else []
+    _link(LIB_PATH, SOURCES, extra, verbose, resource_usage)
+    _link(CEIL_LIB_PATH, CEIL_SOURCES, extra, verbose, resource_usage)
     return LIB_PATH
 
 

@@ -1,6 +1,6 @@
 // C ABI of the attention forward (declared in include/fa.h): host-side argument checks, then kernel
-// launches on the caller's stream (fused forward, split mode, layer-by-layer operators). No
-// allocation, no synchronisation, no global state.
+// launches on the caller's stream (fused forward, split mode, decode-shaped path, layer-by-layer
+// operators). No allocation, no synchronisation, no global state.
 #include <float.h>
 #include <limits.h>
 #include <math.h>
@@ -25,13 +25,14 @@ int64_t split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split) {
   return rows * per_row;
 }
 
-fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
-                    int Sq, int Sk, int d_qk, int d_v, float scale, int causal, hipStream_t stream, int n_split = 0,
-                    void* workspace = nullptr, size_t workspace_bytes = 0) {
+// Checks shared by the fused entry points (fa_fwd_ex, fa_fwd_split and fa_fwd_decode), in the order fa.h documents: sizes, head dimensions, pointers, scale,
+// alignment, index ranges. On FA_OK, *cs holds scale * log2(e) as the kernels take it (magnitude at
+// least FLT_MIN, so that a masked score stays infinite; negative when scale < 0).
+fa_status_t check_fused(const void* Q, const void* K, const void* V, const void* O, const float* LSE, int B, int Hq,
+                        int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal, float* cs) {
   if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0) return FA_ERR_BAD_SHAPE;
   if (Hq > 0 && (Hkv <= 0 || Hq % Hkv != 0)) return FA_ERR_BAD_SHAPE;
-  const int bm = fa::block_rows(d_qk, d_v, causal != 0);
-  if (bm == 0) return FA_ERR_UNSUPPORTED;
+  if (fa::block_rows(d_qk, d_v, causal != 0) == 0) return FA_ERR_UNSUPPORTED;
   // A pointer may be NULL only when the array it addresses has no element.
   const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
   const bool kv_rows = static_cast<int64_t>(B) * Hkv * Sk > 0;
@@ -40,12 +41,24 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
   if (!isfinite(scale)) return FA_ERR_BAD_SCALE;
   const double c = fabs(static_cast<double>(scale)) * 1.4426950408889634074;  // |scale| * log2(e)
   if (c > FLT_MAX) return FA_ERR_BAD_SCALE;
-  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16)) return FA_ERR_UNSUPPORTED;
-  if (!aligned(LSE, 4)) return FA_ERR_UNSUPPORTED;
-  // Offsets inside one head are 32-bit in the kernel.
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(LSE, 4))
+    return FA_ERR_UNSUPPORTED;
+  // Offsets inside one head are 32-bit in the kernels.
   const int64_t dmax = d_qk > d_v ? d_qk : d_v;
   if (static_cast<int64_t>(Sq) * dmax > INT_MAX || static_cast<int64_t>(Sk) * dmax > INT_MAX) return FA_ERR_BAD_SHAPE;
+  const float cmag = c < FLT_MIN ? FLT_MIN : static_cast<float>(c);
+  *cs = scale < 0.f ? -cmag : cmag;
+  return FA_OK;
+}
+
+fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
+                    int Sq, int Sk, int d_qk, int d_v, float scale, int causal, hipStream_t stream, int n_split = 0,
+                    void* workspace = nullptr, size_t workspace_bytes = 0) {
+  float cs = 0.f;
+  const fa_status_t st = check_fused(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, scale, causal, &cs);
+  if (st != FA_OK) return st;
   if (B == 0 || Hq == 0 || Sq == 0) return FA_OK;
+  const int bm = fa::block_rows(d_qk, d_v, causal != 0);
   const int64_t n_qtiles = (static_cast<int64_t>(Sq) + bm - 1) / bm;
   const int64_t n_wg = static_cast<int64_t>(B) * Hq * n_qtiles;
   if (n_wg > INT_MAX || static_cast<int64_t>(B) * Hq > INT_MAX || static_cast<int64_t>(B) * Hkv > INT_MAX)
@@ -70,8 +83,7 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
   p.sq = Sq;
   p.sk = Sk;
   p.group = Hq / Hkv;
-  const float cmag = c < FLT_MIN ? FLT_MIN : static_cast<float>(c);
-  p.cs = scale < 0.f ? -cmag : cmag;
+  p.cs = cs;
   hipError_t err;
   if (n_split > 0) {
     const int64_t rows = static_cast<int64_t>(B) * Hq * Sq;
@@ -85,6 +97,40 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
   return err == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
 
+// Grid checks of the decode-shaped path (after check_fused and the degenerate sizes), and the bytes of
+// partial results it stores (-1 if the count overflows).
+fa_status_t decode_grid(int B, int Hq, int Hkv, int Sq, int d_v, int n_parts, int64_t* need) {
+  const int64_t n_cb = (static_cast<int64_t>(Hq / Hkv) * Sq + 31) / 32;
+  if (static_cast<int64_t>(B) * Hkv * n_cb * n_parts > INT_MAX || static_cast<int64_t>(B) * Hq * Sq > INT_MAX)
+    return FA_ERR_BAD_SHAPE;
+  *need = split_workspace_bytes(B, Hq, Sq, d_v, n_parts);
+  return FA_OK;
+}
+
+hipError_t decode_launch(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq, int Hkv,
+                         int Sq, int Sk, int d_qk, int d_v, float cs, int causal, int n_parts, void* ws,
+                         hipStream_t stream) {
+  fa::DecodeParams p{};
+  p.q = static_cast<const uint16_t*>(Q);
+  p.k = static_cast<const uint16_t*>(K);
+  p.v = static_cast<const uint16_t*>(V);
+  p.o = static_cast<uint16_t*>(O);
+  p.lse = LSE;
+  p.batch = B;
+  p.hq = Hq;
+  p.hkv = Hkv;
+  p.sq = Sq;
+  p.sk = Sk;
+  p.group = Hq / Hkv;
+  p.causal = causal != 0;
+  p.cs = cs;
+  p.rows = p.group * Sq;
+  p.n_parts = n_parts;
+  const int64_t rows = static_cast<int64_t>(B) * Hq * Sq;
+  p.o_part = static_cast<float*>(ws);
+  p.lse_part = p.o_part + rows * n_parts * d_v;
+  return fa::launch_decode(p, d_qk, d_v, stream);
+}
 
 // ---- layer-by-layer operators ------------------------------------------------------------------
 
@@ -154,49 +200,19 @@ fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, 
                           int Sq, int Sk, int d_qk, int d_v, float scale, int causal, int n_parts, void* workspace,
                           size_t workspace_bytes, hipStream_t stream) {
   if (n_parts < 1) return FA_ERR_BAD_SHAPE;
-  if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0) return FA_ERR_BAD_SHAPE;
-  if (Hq > 0 && (Hkv <= 0 || Hq % Hkv != 0)) return FA_ERR_BAD_SHAPE;
-  if (fa::block_rows(d_qk, d_v, causal != 0) == 0) return FA_ERR_UNSUPPORTED;
-  const bool q_rows = static_cast<int64_t>(B) * Hq * Sq > 0;
-  const bool kv_rows = static_cast<int64_t>(B) * Hkv * Sk > 0;
-  if ((q_rows && (Q == nullptr || O == nullptr)) || (kv_rows && (K == nullptr || V == nullptr)))
-    return FA_ERR_NULL_POINTER;
-  if (!isfinite(scale)) return FA_ERR_BAD_SCALE;
-  const double c = fabs(static_cast<double>(scale)) * 1.4426950408889634074;
-  if (c > FLT_MAX) return FA_ERR_BAD_SCALE;
-  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(LSE, 4))
-    return FA_ERR_UNSUPPORTED;
-  const int64_t dmax = d_qk > d_v ? d_qk : d_v;
-  if (static_cast<int64_t>(Sq) * dmax > INT_MAX || static_cast<int64_t>(Sk) * dmax > INT_MAX) return FA_ERR_BAD_SHAPE;
-  if (!q_rows) return FA_OK;
-  const int64_t n_cb = (static_cast<int64_t>(Hq / Hkv) * Sq + 31) / 32;
-  if (static_cast<int64_t>(B) * Hkv * n_cb * n_parts > INT_MAX || static_cast<int64_t>(B) * Hq * Sq > INT_MAX)
-    return FA_ERR_BAD_SHAPE;
-  const int64_t need = split_workspace_bytes(B, Hq, Sq, d_v, n_parts);
+  float cs = 0.f;
+  fa_status_t st = check_fused(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, scale, causal, &cs);
+  if (st != FA_OK) return st;
+  if (static_cast<int64_t>(B) * Hq * Sq == 0) return FA_OK;
+  int64_t need = 0;
+  st = decode_grid(B, Hq, Hkv, Sq, d_v, n_parts, &need);
+  if (st != FA_OK) return st;
   if (need < 0 || workspace == nullptr || static_cast<uint64_t>(need) > workspace_bytes) return FA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return FA_ERR_UNSUPPORTED;
-
-  fa::DecodeParams p{};
-  p.q = static_cast<const uint16_t*>(Q);
-  p.k = static_cast<const uint16_t*>(K);
-  p.v = static_cast<const uint16_t*>(V);
-  p.o = static_cast<uint16_t*>(O);
-  p.lse = LSE;
-  p.batch = B;
-  p.hq = Hq;
-  p.hkv = Hkv;
-  p.sq = Sq;
-  p.sk = Sk;
-  p.group = Hq / Hkv;
-  p.causal = causal != 0;
-  const float cmag = c < FLT_MIN ? FLT_MIN : static_cast<float>(c);
-  p.cs = scale < 0.f ? -cmag : cmag;
-  p.rows = p.group * Sq;
-  p.n_parts = n_parts;
-  const int64_t rows = static_cast<int64_t>(B) * Hq * Sq;
-  p.o_part = static_cast<float*>(workspace);
-  p.lse_part = p.o_part + rows * n_parts * d_v;
-  return fa::launch_decode(p, d_qk, d_v, stream) == hipSuccess ? FA_OK : FA_ERR_HIP;
+  return decode_launch(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, cs, causal, n_parts, workspace, stream) ==
+                 hipSuccess
+             ? FA_OK
+             : FA_ERR_HIP;
 }
 
 int fa_fwd_decode_parts(int n_cu, int B, int Hq, int Hkv, int Sq, int Sk) {

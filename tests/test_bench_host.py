@@ -1,4 +1,5 @@
-"""CPU tests of bench.py's host-side helpers: the traffic figure read from a committed counter summary."""
+"""CPU tests of bench.py's host-side helpers: the traffic figure read from a committed counter summary,
+and the oracle timing (cpu_baseline) on whole heads and on the seeded row subset of long problems."""
 
 import os
 
@@ -38,3 +39,19 @@ def test_committed_summary_has_the_fields_bench_reads():
     recorded = [ln.split(":", 1)[1].strip() for ln in text.splitlines() if ln.startswith("kernel_source_sha256_16:")]
     if recorded == [bench.kernel_source_hash()]:
         assert bench.traffic_from_profile(3) > 0
+
+
+def test_cpu_baseline_whole_heads_and_row_subset():
+    import workloads as W
+
+    small = W.small("cpu baseline small", Hq=4, Hkv=2, Sq=300, Sk=300, causal=True, seed=11)
+    res = bench.cpu_baseline(small, *W.make_inputs(small), budget_s=0.0)
+    # budget 0: exactly one key/value group (2 query heads) is timed, on every row
+    assert res["rows_timed"] == 2 * 300 and "every row" in res["sample"]
+    assert res["value"] > 0 and res["kind"] == "oracle" and res["cores"] >= 1
+    assert res["extrapolated_s"] >= res["measured_s"] * 2 - 1e-3  # scaled by 4 heads / 2 timed
+    long = W.small("cpu baseline long", Hq=1, Hkv=1, Sq=12000, Sk=12000, causal=True, seed=12)
+    res = bench.cpu_baseline(long, *W.make_inputs(long), budget_s=0.0)
+    rows = W.sample_rows(long, n=64)[0]
+    assert res["rows_timed"] == len(rows) and "seeded subsets" in res["sample"]
+    assert abs(res["extrapolated_s"] - res["measured_s"] * 12000 / len(rows)) <= 0.1 + 1e-3 * res["extrapolated_s"]
