@@ -23,8 +23,9 @@
  * LSE[b,h,i] = ln( sum over visible j of exp(scale * q_i . k_j) ), natural log; -inf for a row with
  * no visible key (that row's O is 0).
  *
- * Ownership: the caller owns every buffer. The library allocates nothing, frees nothing, keeps no
- * state beyond its compiled kernels, and is reentrant and thread-safe. Q, K, V are only read; O and
+ * Ownership: the caller owns every buffer. The library allocates nothing, frees nothing, and is
+ * reentrant and thread-safe; its only state is the static scratch array of fa_fwd_decode_noalloc
+ * (below) and that array's per-device address. Q, K, V are only read; O and
  * LSE are only written, every element exactly once per call.
  *
  * Asynchrony: the work is enqueued on `stream` (NULL is the null stream of the current device);
@@ -67,7 +68,8 @@ typedef enum {
   FA_ERR_BAD_SCALE = 4,    /* scale is NaN or +-inf, or |scale| * log2(e) overflows float32       */
   FA_ERR_HIP = 5,          /* the HIP runtime reported an error when enqueuing the kernel         */
   FA_ERR_WORKSPACE = 6     /* split mode: workspace NULL or smaller than                          */
-                           /* fa_fwd_split_workspace_bytes(B, Hq, Sq, d_v, n_split)               */
+                           /* fa_fwd_split_workspace_bytes(B, Hq, Sq, d_v, n_split); for          */
+                           /* fa_fwd_decode_noalloc: that size exceeds FA_NOALLOC_SCRATCH_BYTES   */
 } fa_status_t;
 
 /*
@@ -156,6 +158,36 @@ size_t fa_fwd_split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split)
 fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
                           int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal,
                           int n_parts, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of the static scratch array behind fa_fwd_decode_noalloc (32 MiB per device). */
+#define FA_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/*
+ * fa_fwd_decode_noalloc -- fa_fwd_decode for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same kernels and
+ * results, bit for bit, as fa_fwd_decode with the same n_parts, but the partial results live in a
+ * static device array of FA_NOALLOC_SCRATCH_BYTES that the library holds on every device it runs on
+ * until the process ends, instead of a caller workspace. The call allocates and frees nothing.
+ *
+ *   Q .. causal, n_parts   as in fa_fwd_decode
+ *   stream                 the HIP stream to enqueue on; the scratch of the stream's device is used
+ *                          (the current device's for the NULL stream)
+ *
+ * The first call on a device looks up that device's scratch address (hipGetSymbolAddress), once.
+ * Every call on one device shares its scratch, and every element a call reads there it has written
+ * itself first (nothing needs to start at zero). Calls that overlap in time on one device -- on two
+ * streams, or from two threads without ordering -- race on the scratch and give undefined results;
+ * calls ordered on one stream do not.
+ *
+ * Errors: n_parts < 1 (FA_ERR_BAD_SHAPE); then the checks of fa_fwd_decode in their order up to the
+ * grid size (B*Hq*Sq == 0 returns FA_OK with no HIP call); then partial results of
+ * fa_fwd_split_workspace_bytes(B, Hq, Sq, d_v, n_parts) > FA_NOALLOC_SCRATCH_BYTES bytes
+ * (FA_ERR_WORKSPACE: fewer parts, or fa_fwd_decode with a workspace, is the remedy); a failed lookup
+ * of the scratch address or a failed launch (FA_ERR_HIP).
+ */
+fa_status_t fa_fwd_decode_noalloc(const void* Q, const void* K, const void* V, void* O, float* LSE, int B,
+                                  int Hq, int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale,
+                                  int causal, int n_parts, hipStream_t stream);
 
 /* Suggested n_parts for fa_fwd_decode on a device with n_cu compute units: about one workgroup per
  * CU in total, no part shorter than 4 key tiles (512 keys), at least 1. Host arithmetic only.

@@ -11,7 +11,8 @@ kernel. The functions below marshal arguments and translate status codes, nothin
   :func:`fa_lbl_workspace_bytes`, :func:`fa_fwd_unfused` -- the layer-by-layer (unfused) operators
   and their composition, under the same names.
 * :func:`fa_fwd_decode`, :func:`fa_fwd_decode_parts` -- the decode-shaped path (few query rows per
-  key/value head).
+  key/value head); :func:`fa_fwd_decode_noalloc` -- the same with its partial results in the
+  library's static device scratch, for callers that cannot allocate.
 * :func:`forward` -- convenience wrapper over torch tensors (``n_split`` > 1 selects split mode and
   takes the workspace from torch's allocator; ``decode=True`` the decode-shaped path).
 * :func:`forward_unfused` -- the same over the unfused path (``fa_fwd_unfused``).
@@ -24,12 +25,12 @@ from typing import Optional
 
 from . import _lib
 from ._lib import (FA_ERR_BAD_SCALE, FA_ERR_BAD_SHAPE, FA_ERR_HIP, FA_ERR_NULL_POINTER,  # noqa: F401
-                   FA_ERR_UNSUPPORTED, FA_ERR_WORKSPACE, FA_OK, LIB_PATH)
+                   FA_ERR_UNSUPPORTED, FA_ERR_WORKSPACE, FA_NOALLOC_SCRATCH_BYTES, FA_OK, LIB_PATH)
 
 __all__ = ["fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
            "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
-           "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts", "forward",
-           "forward_unfused", "FaError", "LIB_PATH"]
+           "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts",
+           "fa_fwd_decode_noalloc", "forward", "forward_unfused", "FaError", "LIB_PATH", "FA_NOALLOC_SCRATCH_BYTES"]
 
 
 class FaError(RuntimeError):
@@ -86,6 +87,13 @@ def fa_fwd_decode(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, Hq
     """C ``fa_fwd_decode``: raw device addresses and sizes; returns the status code."""
     return int(_lib.load().fa_fwd_decode(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, float(scale),
                                          int(bool(causal)), int(n_parts), workspace, int(workspace_bytes), stream))
+
+
+def fa_fwd_decode_noalloc(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, Hq: int, Hkv: int, Sq: int,
+                          Sk: int, d_qk: int, d_v: int, scale: float, causal: bool, n_parts: int, stream: int) -> int:
+    """C ``fa_fwd_decode_noalloc``: raw device addresses and sizes; returns the status code."""
+    return int(_lib.load().fa_fwd_decode_noalloc(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, float(scale),
+                                                 int(bool(causal)), int(n_parts), stream))
 
 
 def fa_fwd_decode_parts(n_cu: int, B: int, Hq: int, Hkv: int, Sq: int, Sk: int) -> int:

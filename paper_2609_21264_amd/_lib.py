@@ -21,10 +21,14 @@ FA_ERR_BAD_SCALE = 4
 FA_ERR_HIP = 5
 FA_ERR_WORKSPACE = 6
 
+#: FA_NOALLOC_SCRATCH_BYTES of include/fa.h: the static scratch behind fa_fwd_decode_noalloc.
+FA_NOALLOC_SCRATCH_BYTES = 32 << 20
+
 #: Symbols include/fa.h declares.
 EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
             "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
-            "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts")
+            "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts",
+            "fa_fwd_decode_noalloc")
 
 _lib = None
 
@@ -69,6 +73,8 @@ def load() -> ctypes.CDLL:
     lib.fa_fwd_unfused.restype = i
     lib.fa_fwd_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, i, vp, ctypes.c_size_t, vp]
     lib.fa_fwd_decode.restype = i
+    lib.fa_fwd_decode_noalloc.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, i, vp]
+    lib.fa_fwd_decode_noalloc.restype = i
     lib.fa_fwd_decode_parts.argtypes = [i, i, i, i, i, i]
     lib.fa_fwd_decode_parts.restype = i
     _lib = lib

@@ -1,13 +1,25 @@
 // C ABI of the attention forward (declared in include/fa.h): host-side argument checks, then kernel
 // launches on the caller's stream (fused forward, split mode, decode-shaped path, layer-by-layer
-// operators). No allocation, no synchronisation, no global state.
+// operators). No allocation and no synchronisation; the only state is the per-device address of the
+// static scratch array of fa_fwd_decode_noalloc.
 #include <float.h>
 #include <limits.h>
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "fa.h"
 #include "fa_internal.h"
+
+// Static scratch of the allocation-free decode entry point: fa_fwd_decode_noalloc keeps its partial
+// results in this file-scope device array instead of a caller workspace. Every device the library
+// runs on holds its own copy (allocated with the code object, kept until the process ends). On the
+// host, `scratch` names a host-side stand-in, not a device address: the device address is looked up
+// once per device with hipGetSymbolAddress (with that device current, scratch_for_stream below) and
+// only that address is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[FA_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -25,7 +37,8 @@ int64_t split_workspace_bytes(int B, int Hq, int Sq, int d_v, int n_split) {
   return rows * per_row;
 }
 
-// Checks shared by the fused entry points (fa_fwd_ex, fa_fwd_split and fa_fwd_decode), in the order fa.h documents: sizes, head dimensions, pointers, scale,
+// Checks shared by the fused entry points (fa_fwd_ex, fa_fwd_split, fa_fwd_decode and
+// fa_fwd_decode_noalloc), in the order fa.h documents: sizes, head dimensions, pointers, scale,
 // alignment, index ranges. On FA_OK, *cs holds scale * log2(e) as the kernels take it (magnitude at
 // least FLT_MIN, so that a masked score stays infinite; negative when scale < 0).
 fa_status_t check_fused(const void* Q, const void* K, const void* V, const void* O, const float* LSE, int B, int Hq,
@@ -132,6 +145,45 @@ hipError_t decode_launch(const void* Q, const void* K, const void* V, void* O, f
   return fa::launch_decode(p, d_qk, d_v, stream);
 }
 
+// ---- per-device address of the static scratch (declared at the top of the file) -------------------
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the device `stream` belongs to (the current device for the null
+// stream). The first call on a device looks it up; later calls read the cached address.
+hipError_t scratch_for_stream(hipStream_t stream, void** out) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  int dev = cur;
+  if (stream != nullptr) {
+    e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* ptr = g_scratch[dev].load(std::memory_order_acquire);
+  if (ptr != nullptr) {
+    *out = ptr;
+    return hipSuccess;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  ptr = g_scratch[dev].load(std::memory_order_relaxed);
+  if (ptr == nullptr) {
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess || ptr == nullptr) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+    g_scratch[dev].store(ptr, std::memory_order_release);
+  }
+  *out = ptr;
+  return hipSuccess;
+}
+
 // ---- layer-by-layer operators ------------------------------------------------------------------
 
 int64_t lbl_ld(int Sk) { return (static_cast<int64_t>(Sk) + fa::kLblKeys - 1) / fa::kLblKeys * fa::kLblKeys; }
@@ -210,6 +262,26 @@ fa_status_t fa_fwd_decode(const void* Q, const void* K, const void* V, void* O, 
   if (need < 0 || workspace == nullptr || static_cast<uint64_t>(need) > workspace_bytes) return FA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return FA_ERR_UNSUPPORTED;
   return decode_launch(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, cs, causal, n_parts, workspace, stream) ==
+                 hipSuccess
+             ? FA_OK
+             : FA_ERR_HIP;
+}
+
+fa_status_t fa_fwd_decode_noalloc(const void* Q, const void* K, const void* V, void* O, float* LSE, int B, int Hq,
+                                  int Hkv, int Sq, int Sk, int d_qk, int d_v, float scale, int causal, int n_parts,
+                                  hipStream_t stream) {
+  if (n_parts < 1) return FA_ERR_BAD_SHAPE;
+  float cs = 0.f;
+  fa_status_t st = check_fused(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, scale, causal, &cs);
+  if (st != FA_OK) return st;
+  if (static_cast<int64_t>(B) * Hq * Sq == 0) return FA_OK;
+  int64_t need = 0;
+  st = decode_grid(B, Hq, Hkv, Sq, d_v, n_parts, &need);
+  if (st != FA_OK) return st;
+  if (need < 0 || need > static_cast<int64_t>(FA_NOALLOC_SCRATCH_BYTES)) return FA_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (scratch_for_stream(stream, &ws) != hipSuccess) return FA_ERR_HIP;
+  return decode_launch(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, cs, causal, n_parts, ws, stream) ==
                  hipSuccess
              ? FA_OK
              : FA_ERR_HIP;

@@ -354,6 +354,51 @@ def test_decode_parts_heuristic(lib):
         assert fa.fa_fwd_decode_parts(*args) == 0
 
 
+# ---- allocation-free decode entry point: host-side checks only ------------------------------------
+
+def call_noalloc(**kw):
+    a = dict(Q=QP, K=KP, V=VP, O=OP, LSE=LP, B=1, Hq=32, Hkv=8, Sq=1, Sk=4096, d_qk=128, d_v=128,
+             scale=0.125, causal=0, n_parts=4, stream=None)
+    a.update(kw)
+    return fa.fa_fwd_decode_noalloc(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["B"], a["Hq"], a["Hkv"], a["Sq"],
+                                    a["Sk"], a["d_qk"], a["d_v"], a["scale"], a["causal"], a["n_parts"], a["stream"])
+
+
+def test_noalloc_scratch_size_matches_header(lib):
+    m = re.search(r"#define\s+FA_NOALLOC_SCRATCH_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == fa.FA_NOALLOC_SCRATCH_BYTES
+
+
+# Largest partial-result count that fits: rows * n_parts * (d_v + 1) * 4 <= 32 MiB.
+_ROWS_FIT = fa.FA_NOALLOC_SCRATCH_BYTES // (129 * 4)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_parts=0), fa.FA_ERR_BAD_SHAPE),
+    (dict(n_parts=0, Q=None), fa.FA_ERR_BAD_SHAPE),
+    (dict(Hkv=5), fa.FA_ERR_BAD_SHAPE),
+    (dict(d_qk=96, d_v=96), fa.FA_ERR_UNSUPPORTED),
+    (dict(K=None), fa.FA_ERR_NULL_POINTER),
+    (dict(scale=float("nan")), fa.FA_ERR_BAD_SCALE),
+    (dict(V=VP + 4), fa.FA_ERR_UNSUPPORTED),
+    (dict(Sk=20_000_000), fa.FA_ERR_BAD_SHAPE),
+    (dict(B=1, Hq=4096, Hkv=4096, Sq=1, n_parts=2 ** 20), fa.FA_ERR_BAD_SHAPE),
+    # partial results one row past the scratch (B*Hq*Sq rows, one part): rejected before any HIP call
+    (dict(B=1, Hq=1, Hkv=1, Sq=_ROWS_FIT + 1, n_parts=1), fa.FA_ERR_WORKSPACE),
+    (dict(B=1, Hq=32, Hkv=8, Sq=64, n_parts=_ROWS_FIT // (32 * 64) + 1), fa.FA_ERR_WORKSPACE),
+    # an invalid argument still wins over the size
+    (dict(B=1, Hq=1, Hkv=1, Sq=_ROWS_FIT + 1, n_parts=1, scale=float("inf")), fa.FA_ERR_BAD_SCALE),
+])
+def test_noalloc_invalid_arguments_are_rejected_on_host(lib, kw, status):
+    assert call_noalloc(**kw) == status
+
+
+def test_noalloc_empty_problems_are_noops_without_hip(lib):
+    assert call_noalloc(B=0) == fa.FA_OK
+    assert call_noalloc(Sq=0, Q=None, O=None) == fa.FA_OK
+    assert call_noalloc(Hq=0, Hkv=0) == fa.FA_OK
+
+
 def _compile(cmd, source, suffix, tmp_path):
     path = tmp_path / f"t{suffix}"
     path.write_text(source)
