@@ -273,7 +273,10 @@ fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
 /* Static, human-readable name of a status code ("FA_OK", ...); "unknown status" otherwise. */
 const char* fa_status_str(fa_status_t s);
 
-/* Number of query rows one workgroup processes for the given head dimensions (0 if unsupported). */
+/* Query rows per workgroup of the fused kernel for the given head dimensions, as split mode and
+ * problems with more than 256 such blocks (B * Hq * ceil(Sq / rows)) run it; 0 if unsupported.
+ * Other problems at (d_qk, d_v) = (64, 64) or (128, 128) run workgroups of half as many rows, two
+ * per compute unit, so that few query blocks still occupy the GPU. Host arithmetic only. */
 int fa_block_rows(int d_qk, int d_v, int causal);
 
 #ifdef __cplusplus

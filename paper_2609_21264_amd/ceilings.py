@@ -2,8 +2,9 @@
 
 Runs the microbenchmarks of ``libfa_ceilings.so`` (``csrc/fa_ceilings.hip``) and prints one JSON
 line: the bf16 MFMA rate with nothing else to do at one and two waves per SIMD, and the shader clock
-the chip sustains meanwhile (the counterpart of the paper's instruction-count compute ceiling, Sec.
-5.2); HBM streaming reads through VGPRs and through direct-to-LDS buffer loads, 2 GiB each, far past
+the chip sustains meanwhile; the cycles an MFMA slot takes with the online softmax's VALU work
+(exponentials, fmas) issued next to it (together the counterpart of the paper's instruction-count
+compute ceiling, Sec. 5.2); HBM streaming reads through VGPRs and through direct-to-LDS buffer loads, 2 GiB each, far past
 the 256 MB Infinity Cache (the per-level bandwidth ceilings of Sec. 5.2 / Table 2); and the LDS read
 rate of the two read forms the fused kernel uses, in bytes per clock per CU.
 
@@ -27,6 +28,8 @@ PEAK_BF16_TFLOPS = 2516.6  # 256 CUs x 4096 dense bf16 FLOP/clk/CU x 2.4 GHz
 PEAK_HBM_GBS = 8000.0
 NOMINAL_CLOCK_GHZ = 2.4
 MFMA_FLOP = 2 * 32 * 32 * 16  # one v_mfma_f32_32x32x16_bf16
+# (v_exp_f32, v_fma_f32) per MFMA slot of fa_ceil_mix (FA_CEIL_MIXES in fa_ceilings.hip)
+MIXES = [(0, 0), (0, 2), (0, 4), (0, 6), (0, 8), (1, 0), (2, 0), (1, 2), (1, 3), (1, 4), (2, 2), (2, 4)]
 
 _lib = None
 
@@ -42,10 +45,11 @@ def load() -> ctypes.CDLL:
     lib = ctypes.CDLL(_build.CEIL_LIB_PATH)
     vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
     lib.fa_ceil_mfma.argtypes = [vp, vp, vp, i, i, i, vp]
+    lib.fa_ceil_mix.argtypes = [vp, vp, vp, i, i, i, i, i, vp]
     lib.fa_ceil_read_vgpr.argtypes = [vp, sz, vp, vp, i, vp]
     lib.fa_ceil_read_lds.argtypes = [vp, sz, vp, i, vp]
     lib.fa_ceil_lds.argtypes = [vp, vp, i, i, i, vp]
-    for f in (lib.fa_ceil_mfma, lib.fa_ceil_read_vgpr, lib.fa_ceil_read_lds, lib.fa_ceil_lds):
+    for f in (lib.fa_ceil_mfma, lib.fa_ceil_mix, lib.fa_ceil_read_vgpr, lib.fa_ceil_read_lds, lib.fa_ceil_lds):
         f.restype = i
     _lib = lib
     return lib
@@ -117,6 +121,28 @@ def main(repeats: int = 5) -> dict:
             "ms": round(ms, 3), "realtime_counter_mhz": round(real_hz / 1e6, 2)}
         print(f"[ceilings] mfma {wpe} wave/SIMD: best {tflops:.1f} TFLOP/s at {ghz:.3f} GHz, last {last:.1f} at "
               f"{last_ghz:.3f} GHz", file=sys.stderr, flush=True)
+
+    # Issue cost of VALU work next to the MFMAs: shader cycles per slot (one MFMA plus n_exp
+    # v_exp_f32 and n_fma v_fma_f32) per SIMD, at one and two waves per SIMD. An MFMA alone is 32
+    # cycles of matrix-core work; a slot longer than that is bound by instruction issue.
+    mix = {}
+    for wpe in (1, 2):
+        out = torch.empty(n_cu * 256 * wpe, dtype=torch.float32, device=dev)
+        stamps = torch.zeros(n_cu * 4 * wpe * 4, dtype=torch.int64, device=dev)
+        for ne, nf in MIXES:
+            iters = 4096
+            runs = _timed(lambda: lib.fa_ceil_mix(ops.data_ptr(), out.data_ptr(), stamps.data_ptr(), wpe, ne, nf, n_cu,
+                                                  iters, handle), stamps, 3)
+            # per workgroup (one CU, wpe waves per SIMD): first start to last end of its waves, over
+            # the slots one SIMD runs (the waves of a SIMD do not share it evenly: one runs ahead)
+            s_ = stamps.view(n_cu, 4 * wpe, 4).to(torch.float64).cpu()
+            span = s_[:, :, 1].max(dim=1).values - s_[:, :, 0].min(dim=1).values
+            cyc = float(span.median()) / (iters * 4 * wpe)
+            mix[f"{wpe}wave_{ne}exp_{nf}fma"] = round(cyc, 2)
+        print(f"[ceilings] mix {wpe} wave/SIMD: " + ", ".join(f"{k.split('_', 1)[1]} {v}" for k, v in mix.items()
+                                                              if k.startswith(f"{wpe}wave")),
+              file=sys.stderr, flush=True)
+    res["mfma_valu_mix_cycles_per_slot_per_simd"] = mix
 
     # HBM streaming reads, 2 GiB (past the Infinity Cache).
     nbytes = 2 << 30

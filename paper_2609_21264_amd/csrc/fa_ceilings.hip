@@ -17,6 +17,9 @@
 //       LDS so that one workgroup occupies a CU; every wave runs iters x 16 v_mfma_f32_32x32x16_bf16
 //       on 4 independent accumulators from operands (bf16, >= 1024 elements, 16-byte aligned).
 //       out: n_wg * 256 * waves_per_simd floats; stamps: 4 per wave.
+//   fa_ceil_mix(operands, out, stamps, waves_per_simd, n_exp, n_fma, n_wg, iters, stream)
+//       as fa_ceil_mfma, but each MFMA is followed by n_exp v_exp_f32 and n_fma v_fma_f32 (independent
+//       of the MFMAs); (n_exp, n_fma) one of the pairs of FA_CEIL_MIXES.
 //   fa_ceil_read_vgpr(src, bytes, out, stamps, n_wg, stream)
 //       reads src[0, bytes) once with 16-byte loads into VGPRs (grid-stride, coalesced);
 //       bytes a positive multiple of 16, src 16-byte aligned; out: 16 bytes (written only in the
@@ -30,6 +33,7 @@
 //       ds_read_b64_tr_b16 of 512 bytes with the fused kernel's V-tile addressing (transpose = 1)
 //       per pass, conflict-free; out: n_wg * 256 * 4 uint32.
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 #include "fa_device.h"
@@ -85,6 +89,50 @@ void ceil_mfma_kernel(const uint16_t* __restrict__ operands, float* __restrict__
 #pragma unroll
   for (int r = 0; r < 16; ++r) s += c0[r] + c1[r] + c2[r] + c3[r];
   // touch the LDS reservation so that it is kept (one byte per workgroup, written and read back)
+  if (threadIdx.x == 0) hold[blockIdx.x % kMfmaLds] = (unsigned char)iters;
+  __syncthreads();
+  out[blockIdx.x * blockDim.x + threadIdx.x] = s + (float)hold[blockIdx.x % kMfmaLds];
+}
+
+// Issue cost of the online softmax's VALU work next to the MFMAs (the counterpart of the paper's
+// instruction-count ceiling): every slot is one v_mfma_f32_32x32x16_bf16 (4 independent accumulators
+// in turn) followed by NE v_exp_f32 and NF v_fma_f32 on 16 independent registers (each register is
+// updated once per 4 slots when NE + NF = 4), issued in exactly this order. The stamps give the
+// shader cycles per slot.
+template <int WPE, int NE, int NF>
+__global__ __attribute__((amdgpu_flat_work_group_size(256 * WPE, 256 * WPE), amdgpu_waves_per_eu(WPE, WPE)))
+void ceil_mix_kernel(const uint16_t* __restrict__ operands, float* __restrict__ out, uint64_t* __restrict__ stamps,
+                     int iters) {
+  __shared__ unsigned char hold[kMfmaLds];
+  const int lane = threadIdx.x & 63;
+  const bf16x8 a = *reinterpret_cast<const bf16x8*>(operands + lane * 8);
+  const bf16x8 b = *reinterpret_cast<const bf16x8*>(operands + 512 + lane * 8);
+  f32x16 c[4] = {};
+  float x[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) x[k] = 0.0625f * (float)(k + 1) + 0.001f * (float)lane;
+  uint64_t clk0, real0;
+  stamp_begin(clk0, real0);
+  // Volatile asm statements keep their order; no instruction reads a register another one wrote
+  // within the same slot, so no wait states are needed.
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c[u]) : "v"(a), "v"(b));
+#pragma unroll
+      for (int e = 0; e < NE; ++e) asm volatile("v_exp_f32 %0, -|%0|" : "+v"(x[(u * (NE + NF) + e) & 15]));
+#pragma unroll
+      for (int f = 0; f < NF; ++f) asm volatile("v_fma_f32 %0, %0, 0.5, 0.5" : "+v"(x[(u * (NE + NF) + NE + f) & 15]));
+    }
+  }
+  stamp_end(stamps, clk0, real0);
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) s += x[k];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += c[u][r];
   if (threadIdx.x == 0) hold[blockIdx.x % kMfmaLds] = (unsigned char)iters;
   __syncthreads();
   out[blockIdx.x * blockDim.x + threadIdx.x] = s + (float)hold[blockIdx.x % kMfmaLds];
@@ -187,6 +235,29 @@ int fa_ceil_mfma(const void* operands, float* out, unsigned long long* stamps, i
   else
     hipLaunchKernelGGL(ceil_mfma_kernel<2>, dim3(n_wg), dim3(512), 0, stream, op, out, st, iters);
   return hipGetLastError();
+}
+
+// Instruction mixes of fa_ceil_mix: (exponentials, fmas) per MFMA slot.
+#define FA_CEIL_MIXES(X) X(0, 0) X(0, 2) X(0, 4) X(0, 6) X(0, 8) X(1, 0) X(2, 0) X(1, 2) X(1, 3) X(1, 4) X(2, 2) X(2, 4)
+
+int fa_ceil_mix(const void* operands, float* out, unsigned long long* stamps, int waves_per_simd, int n_exp,
+                int n_fma, int n_wg, int iters, hipStream_t stream) {
+  if (operands == nullptr || out == nullptr || stamps == nullptr || n_wg <= 0 || iters <= 0 ||
+      (reinterpret_cast<uintptr_t>(operands) & 15) != 0 || (waves_per_simd != 1 && waves_per_simd != 2))
+    return hipErrorInvalidValue;
+  const uint16_t* op = static_cast<const uint16_t*>(operands);
+  uint64_t* st = reinterpret_cast<uint64_t*>(stamps);
+#define FA_CEIL_MIX_CASE(E, F)                                                                          \
+  if (n_exp == E && n_fma == F) {                                                                       \
+    if (waves_per_simd == 1)                                                                            \
+      hipLaunchKernelGGL((ceil_mix_kernel<1, E, F>), dim3(n_wg), dim3(256), 0, stream, op, out, st, iters); \
+    else                                                                                                \
+      hipLaunchKernelGGL((ceil_mix_kernel<2, E, F>), dim3(n_wg), dim3(512), 0, stream, op, out, st, iters); \
+    return hipGetLastError();                                                                           \
+  }
+  FA_CEIL_MIXES(FA_CEIL_MIX_CASE)
+#undef FA_CEIL_MIX_CASE
+  return hipErrorInvalidValue;
 }
 
 int fa_ceil_read_vgpr(const void* src, size_t bytes, void* out, unsigned long long* stamps, int n_wg,

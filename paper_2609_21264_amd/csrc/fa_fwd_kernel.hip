@@ -46,21 +46,6 @@
 namespace fa {
 namespace {
 
-#ifndef FA_KPF
-#define FA_KPF 2
-#endif
-#ifndef FA_VPF
-#define FA_VPF 6
-#endif
-// K and V ring slots (tiles resident in LDS per workgroup). Loading K only two tiles ahead measured
-// 2-3 % faster than three on the 8K, 4K-d192 and 128K prefill shapes (one box, interleaved).
-#ifndef FA_NKR
-#define FA_NKR 2
-#endif
-#ifndef FA_NVR
-#define FA_NVR 4
-#endif
-
 constexpr float kLn2 = 0.69314718055994530942f;
 // A tile's exponentials are accepted when every lane's sum of them is at most 2^8: then no
 // probability exceeds 2^8 relative to the reference maximum.
@@ -85,34 +70,67 @@ __device__ __forceinline__ int o_half(int r) { return DV >= 128 ? ((r ^ (r >> 4)
 //    rescale, epilogue) in both directions: 18 wait states cover the MFMA write-to-read distance,
 //    and the operand tie keeps the order;
 //  * consecutive MFMAs accumulating into exactly the same registers need no wait states.
+// AG selects where O and Q live: AGPRs (one wave per SIMD, where the VGPRs alone cannot hold the
+// step's scores, probabilities and fragments next to them) or VGPRs (two waves per SIMD: the
+// compiler splits a wave's 256 registers evenly between the two files as soon as any AGPR is used,
+// which would leave 128 VGPRs for the step; with no AGPR all 256 are VGPRs).
+template <bool AG>
 __device__ __forceinline__ void mfma_out(f32x16& acc, const bf16x8& v, const bf16x8& pt) {
-  asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(pt));
+  if constexpr (AG)
+    asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(pt));
+  else
+    asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(v), "v"(pt));
 }
 // Same without the leading wait states, for operands no VALU instruction has written recently: in
 // the pipelined step, P was packed a whole step earlier and V comes from LDS.
+template <bool AG>
 __device__ __forceinline__ void mfma_out_settled(f32x16& acc, const bf16x8& v, const bf16x8& pt) {
-  asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(pt));
+  if constexpr (AG)
+    asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(pt));
+  else
+    asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(v), "v"(pt));
 }
+template <bool AG>
 __device__ __forceinline__ void agpr_fence(f32x16& acc) {
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+a"(acc));
+  if constexpr (AG)
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+a"(acc));
+  else
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(acc));
 }
-// 16 bytes of Q straight into an AGPR tuple (only read as an MFMA operand, so it never needs a VGPR
+// 16 bytes of Q straight into its register tuple (only read as an MFMA operand, so it never needs a
 // copy). The load is not waited for here: the caller waits on vmcnt and then passes the value
 // through q_ready(), which keeps every read of it after that wait.
+template <bool AG>
 __device__ __forceinline__ void load_q(bf16x8& r, const void* ptr) {
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=a"(r) : "v"(ptr) : "memory");
+  if constexpr (AG)
+    asm volatile("global_load_dwordx4 %0, %1, off" : "=a"(r) : "v"(ptr) : "memory");
+  else
+    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(ptr) : "memory");
 }
-__device__ __forceinline__ void q_ready(bf16x8& r) { asm volatile("" : "+a"(r)); }
+template <bool AG>
+__device__ __forceinline__ void q_ready(bf16x8& r) {
+  if constexpr (AG)
+    asm volatile("" : "+a"(r));
+  else
+    asm volatile("" : "+v"(r));
+}
 
-template <int DQK_, int DV_, int BN_, int NWAVES_, int QB_, bool CAUSAL_, bool SPLIT_>
+// Compile-time configuration of one kernel instance: head dimensions, key-tile width, waves per
+// workgroup, 32-row query blocks per wave, causal masking, split mode, workgroups sharing a CU (OCC),
+// K and V fragments read ahead from LDS (KPF, VPF), and K and V ring slots in LDS (NKR, NVR).
+template <int DQK_, int DV_, int BN_, int NWAVES_, int QB_, bool CAUSAL_, bool SPLIT_, int OCC_, int KPF_, int VPF_,
+          int NKR_, int NVR_>
 struct Cfg {
   static constexpr int DQK = DQK_, DV = DV_, BN = BN_, NWAVES = NWAVES_, QB = QB_;
+  static constexpr int KPF = KPF_, VPF = VPF_;
   static constexpr bool CAUSAL = CAUSAL_;
   // SPLIT: each workgroup takes one of n_split contiguous parts of its query block's key tiles and
   // writes a partial result (O normalised by its own row sum, fp32, and its LSE) for a merge pass.
   static constexpr bool SPLIT = SPLIT_;
   static constexpr int NT = NWAVES * 64;
-  static constexpr int WPE = NWAVES > 4 ? NWAVES / 4 : 1;  // waves per SIMD (4 SIMDs per CU)
+  // Waves per SIMD the registers are budgeted for: the workgroup's own (4 SIMDs per CU) times the
+  // workgroups that share a CU (OCC_).
+  static constexpr int WPE = (NWAVES > 4 ? NWAVES / 4 : 1) * OCC_;
   static constexpr int BM = NWAVES * 32 * QB;  // query rows per workgroup
   static constexpr int KCH = DQK / 8;          // 16-byte chunks per K-tile row
   static constexpr int VCH = DV / 8;           // 16-byte chunks per V-tile row
@@ -120,7 +138,7 @@ struct Cfg {
   static constexpr int V_BYTES = BN * DV * 2;
   // Ring slots. Step j loads K(j + KA) into the slot of K(j) and V(j + VA) into the slot of V(j-2):
   // both were last read in step j-1, which every wave has finished at the barrier of step j.
-  static constexpr int NKR = FA_NKR, NVR = FA_NVR;
+  static constexpr int NKR = NKR_, NVR = NVR_;
   static constexpr int KA = NKR, VA = NVR - 2;  // how far ahead step j loads K and V tiles
   static constexpr int LDS_BYTES = NKR * K_BYTES + NVR * V_BYTES;
   // Direct-to-LDS loads per wave per tile (each moves 64 lanes x 16 bytes).
@@ -133,7 +151,7 @@ struct Cfg {
   // prologue's groups j = -KA .. -1 hold every tile's first load.
   static_assert(NKR >= 2 && NKR + 1 <= NVR && NVR <= NKR + 2, "ring sizes");
   static_assert(KA * (K_LOADS + V_LOADS) < 64 && VA * (K_LOADS + V_LOADS) < 64, "vmcnt range");
-  static_assert(LDS_BYTES <= 163840, "LDS budget");
+  static_assert(LDS_BYTES * OCC_ <= 163840, "LDS budget of the workgroups sharing a CU");
 };
 
 // Map a hardware workgroup index to (batch, query head, query block). Workgroup t runs on XCD
@@ -183,10 +201,11 @@ struct Attn {
   static constexpr int NMS = KS * KB * QB;  // score MFMAs per tile
   static constexpr int NMP = PS * DB * QB;  // P V MFMAs per tile
   static constexpr int NSL = NMS + NMP;     // MFMA slots per step
+  static constexpr bool AG = C::WPE == 1;   // O and Q in AGPRs
   static constexpr int NEP = KB * QB * 8;   // exponential pairs per lane per tile
   static constexpr int NVF = PS * DB;       // V fragments per tile
-  static constexpr int KPF = FA_KPF;        // K fragments read ahead
-  static constexpr int VPF = FA_VPF;        // V fragments read ahead
+  static constexpr int KPF = C::KPF;        // K fragments read ahead
+  static constexpr int VPF = C::VPF;        // V fragments read ahead
 
   int i32, h, qw, diag, sk;
   const uint16_t* kg;  // this workgroup's K head in global memory (rebase only)
@@ -306,9 +325,9 @@ struct Attn {
     const int kb = ps >> 1, base = (ps & 1) * 4;
     const u32x4 w = {pk[kb][qb][base], pk[kb][qb][base + 1], pk[kb][qb][base + 2], pk[kb][qb][base + 3]};
     if (settled)
-      mfma_out_settled(oacc[db][qb], vf[t], bit_cast<bf16x8>(w));
+      mfma_out_settled<AG>(oacc[db][qb], vf[t], bit_cast<bf16x8>(w));
     else
-      mfma_out(oacc[db][qb], vf[t], bit_cast<bf16x8>(w));
+      mfma_out<AG>(oacc[db][qb], vf[t], bit_cast<bf16x8>(w));
   }
 
   // All P V MFMAs of one tile (the last tile, after the loop).
@@ -348,9 +367,9 @@ struct Attn {
       l_run[qb] *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        agpr_fence(oacc[db][qb]);
+        agpr_fence<AG>(oacc[db][qb]);
         oacc[db][qb] *= alpha;
-        agpr_fence(oacc[db][qb]);
+        agpr_fence<AG>(oacc[db][qb]);
       }
       mref[qb] = m_new == -INFINITY ? 0.f : m_new;
       rs[qb] = 0.f;
@@ -477,7 +496,7 @@ void fa_fwd_kernel(FwdParams p) {
   for (int qb = 0; qb < QB; ++qb) {
     const int row = min(st.qw + qb * 32 + st.i32, p.sq - 1);
 #pragma unroll
-    for (int ks = 0; ks < A::KS; ++ks) load_q(st.qf[qb][ks], qh + (size_t)row * DQK + ks * 16 + st.h * 8);
+    for (int ks = 0; ks < A::KS; ++ks) load_q<A::AG>(st.qf[qb][ks], qh + (size_t)row * DQK + ks * 16 + st.h * 8);
   }
 
   // Rings: step j loads K(j+KA) and V(j+VA) (the group of step j); the prologue loads the groups of
@@ -502,7 +521,7 @@ void fa_fwd_kernel(FwdParams p) {
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int ks = 0; ks < A::KS; ++ks) q_ready(st.qf[qb][ks]);
+    for (int ks = 0; ks < A::KS; ++ks) q_ready<A::AG>(st.qf[qb][ks]);
 
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -511,7 +530,7 @@ void fa_fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int db = 0; db < A::DB; ++db) {
       st.oacc[db][qb] = f32x16{};
-      agpr_fence(st.oacc[db][qb]);
+      agpr_fence<A::AG>(st.oacc[db][qb]);
     }
   }
 
@@ -609,7 +628,7 @@ void fa_fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-      for (int db = 0; db < A::DB; ++db) agpr_fence(st.oacc[db][qb]);
+      for (int db = 0; db < A::DB; ++db) agpr_fence<A::AG>(st.oacc[db][qb]);
     const size_t head_rows = ((size_t)split * p.batch * p.hq + (size_t)b * p.hq + hq) * p.sq;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -638,7 +657,7 @@ void fa_fwd_kernel(FwdParams p) {
   #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
   #pragma unroll
-      for (int db = 0; db < A::DB; ++db) agpr_fence(st.oacc[db][qb]);
+      for (int db = 0; db < A::DB; ++db) agpr_fence<A::AG>(st.oacc[db][qb]);
     {
       const int osw = o_swizzle<DV>(st.i32) << 4;             // qb * 32 leaves the low 5 row bits alone
       const int ohalf = (st.h ^ o_half<DV>(st.i32)) << 3;
@@ -692,9 +711,18 @@ void fa_fwd_kernel(FwdParams p) {
   }
 }
 
-// Tile configuration (compile-time): key-tile width, waves per workgroup, 32-row query blocks per
-// wave. One wave per SIMD; the register budget of a wave (O 128 + Q 64 AGPRs at d = 128, two score
-// tiles and P in VGPRs) is what fixes 64 query rows per wave.
+// The two instances. Long: 4 waves x 64 query rows (256 rows per workgroup), one workgroup per CU,
+// one wave per SIMD; the register budget of a wave (O 128 + Q 64 AGPRs at d = 128, two score tiles
+// and P in VGPRs) is what fixes 64 query rows per wave. K tiles are loaded two ahead: a third K slot
+// measured 2-3 % slower on the 8K, 4K-d192 and 128K prefill shapes (one box, interleaved).
+// Short: 4 waves x 32 query rows (128 rows per workgroup), two workgroups per CU (two waves per SIMD,
+// 256 registers each, O and Q in VGPRs), a 3-slot V ring so that two rings fit one CU's LDS, and
+// shallower fragment prefetch at d = 128 so that the step fits the registers without spilling. It
+// runs problems with few query blocks (short sequences, few heads), where 256-row blocks leave CUs
+// idle and each block's serial chain of steps sets the time: on the paper's S = 512 and 2048 GPT-2
+// and BERT shapes and the 128K single-head workload it measured 1.2-1.4x faster than the long
+// instance, and slower once the long instance's grid fills the GPU. At d_qk = 192 two waves per SIMD
+// do not fit, so those problems always run the long instance.
 #ifndef FA_BN
 #define FA_BN 64
 #endif
@@ -704,30 +732,68 @@ void fa_fwd_kernel(FwdParams p) {
 #ifndef FA_QB
 #define FA_QB 2
 #endif
+#ifndef FA_KPF
+#define FA_KPF 2
+#endif
+#ifndef FA_VPF
+#define FA_VPF 6
+#endif
+#ifndef FA_NKR
+#define FA_NKR 2
+#endif
+#ifndef FA_NVR
+#define FA_NVR 4
+#endif
 
 template <int DQK, int DV, bool CAUSAL, bool SPLIT = false>
 struct Instance {
-  using C = Cfg<DQK, DV, FA_BN, FA_NWAVES, FA_QB, CAUSAL, SPLIT>;
+  using C = Cfg<DQK, DV, FA_BN, FA_NWAVES, FA_QB, CAUSAL, SPLIT, 1, FA_KPF, FA_VPF, FA_NKR, FA_NVR>;
+};
+template <int DQK, int DV, bool CAUSAL>
+struct ShortInstance {
+  using C = Cfg<DQK, DV, 64, 4, 1, CAUSAL, false, 2, DQK >= 128 ? 1 : 2, DQK >= 128 ? 2 : 6, 2, 3>;
 };
 
-template <int DQK, int DV, bool CAUSAL, bool SPLIT>
-hipError_t launch_instance(FwdParams p, hipStream_t stream) {
-  using C = typename Instance<DQK, DV, CAUSAL, SPLIT>::C;
+// Largest grid of long-instance workgroups (256-row blocks) that runs the short instance instead:
+// the CU count of MI355X, so that the long instance would leave CUs idle.
+constexpr int64_t kShortMaxBlocks = 256;
+
+bool use_short(const FwdParams& p, int d_qk, int d_v) {
+  if (!((d_qk == 64 && d_v == 64) || (d_qk == 128 && d_v == 128))) return false;
+  const int bm = Instance<64, 64, false>::C::BM;
+  const int64_t blocks = (int64_t)p.batch * p.hq * ((p.sq + bm - 1) / bm);
+  return blocks <= kShortMaxBlocks;
+}
+
+template <class C>
+hipError_t launch_cfg(FwdParams p, hipStream_t stream) {
   p.n_qtiles = (p.sq + C::BM - 1) / C::BM;
   p.n_wg = p.batch * p.hq * p.n_qtiles;
   void* args[] = {&p};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel<C>), dim3(p.n_wg * (SPLIT ? p.n_split : 1)),
+  return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel<C>), dim3(p.n_wg * (C::SPLIT ? p.n_split : 1)),
                          dim3(C::NT), args, 0, stream);
+}
+
+template <int DQK, int DV, bool CAUSAL, bool SPLIT>
+hipError_t launch_instance(FwdParams p, bool short_blocks, hipStream_t stream) {
+  if constexpr (!SPLIT && DQK != 192) {
+    if (short_blocks) return launch_cfg<typename ShortInstance<DQK, DV, CAUSAL>::C>(p, stream);
+  }
+  return launch_cfg<typename Instance<DQK, DV, CAUSAL, SPLIT>::C>(p, stream);
 }
 
 template <bool SPLIT>
 hipError_t launch_dims(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream) {
+  const bool sh = !SPLIT && use_short(p, d_qk, d_v);
   if (d_qk == 64 && d_v == 64)
-    return causal ? launch_instance<64, 64, true, SPLIT>(p, stream) : launch_instance<64, 64, false, SPLIT>(p, stream);
+    return causal ? launch_instance<64, 64, true, SPLIT>(p, sh, stream)
+                  : launch_instance<64, 64, false, SPLIT>(p, sh, stream);
   if (d_qk == 128 && d_v == 128)
-    return causal ? launch_instance<128, 128, true, SPLIT>(p, stream) : launch_instance<128, 128, false, SPLIT>(p, stream);
+    return causal ? launch_instance<128, 128, true, SPLIT>(p, sh, stream)
+                  : launch_instance<128, 128, false, SPLIT>(p, sh, stream);
   if (d_qk == 192 && d_v == 128)
-    return causal ? launch_instance<192, 128, true, SPLIT>(p, stream) : launch_instance<192, 128, false, SPLIT>(p, stream);
+    return causal ? launch_instance<192, 128, true, SPLIT>(p, sh, stream)
+                  : launch_instance<192, 128, false, SPLIT>(p, sh, stream);
   return hipErrorInvalidValue;
 }
 

@@ -39,7 +39,9 @@ struct MergeParams {
   int n_split;
 };
 
-// Query rows per workgroup of the kernel instance for (d_qk, d_v, causal); 0 if not compiled in.
+// Query rows per workgroup of the long kernel instance for (d_qk, d_v, causal) (split mode, and
+// problems with more than 256 such blocks); 0 if not compiled in. Problems with fewer blocks at
+// d = 64 or 128 run the short instance, with half as many rows per workgroup.
 int block_rows(int d_qk, int d_v, bool causal);
 
 // Enqueue the forward kernel for (d_qk, d_v, causal) on `stream`. Requires Sq > 0, B*Hq > 0 and a

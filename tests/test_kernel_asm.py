@@ -1,8 +1,9 @@
 """Static checks of the gfx950 assembly hipcc generates for the kernels (no GPU needed).
 
-* The fused kernel's P V MFMAs are written as inline assembly, so the compiler's hazard recognizer
-  does not pad them: where the kernel omits the wait states in front of such an MFMA it relies on no
-  VALU instruction having written one of its source registers just before. gfx950 needs two wait
+* The fused kernel's P V MFMAs are written as inline assembly (accumulating into AGPRs in the
+  long instance, into VGPRs in the short one), so the compiler's hazard recognizer does not pad them:
+  where the kernel omits the wait states in front of such an MFMA it relies on no VALU instruction
+  having written one of its source registers just before. gfx950 needs two wait
   states between a VALU write of a VGPR and an MFMA that reads it; this is checked in the code.
 * Some loads into registers are inline assembly the compiler does not track (Q in the fused kernel,
   P in the layer-by-layer P V kernel): the kernels order them with explicit vmcnt waits. The check
@@ -77,37 +78,6 @@ def _instructions(text):
             continue  # directives; local labels (".LBB0_1:") are kept
         out.append(("label", s) if s.endswith(":") else ("ins", s))
     return out
-
-
-def test_agpr_mfma_operands_settled(asm_text):
-    ins = _instructions(asm_text)
-    checked, problems = 0, []
-    for i, (kind, s) in enumerate(ins):
-        if kind != "ins" or not s.startswith("v_mfma"):
-            continue
-        ops = [o.strip() for o in s.split(None, 1)[1].split(",")]
-        if not ops[0].startswith("a"):
-            continue  # VGPR-form MFMAs are emitted (and padded) by the compiler itself
-        checked += 1
-        srcs = _regs(ops[1]) | _regs(ops[2]) | _regs(ops[3])
-        ws, j = 0, i - 1
-        while j >= 0 and ws < WAIT_STATES:
-            k, t = ins[j]
-            if k == "label":
-                problems.append(f"branch target within {WAIT_STATES} wait states of: {s}")
-                break
-            if t.startswith("s_nop"):
-                ws += int(t.split()[1]) + 1
-            else:
-                op = t.split()[0]
-                if op.startswith("v_") and not op.startswith("v_mfma") and " " in t:
-                    dst = t.split(None, 1)[1].split(",")[0].strip()
-                    if _regs(dst) & srcs:
-                        problems.append(f"{t}  ->  {s}")
-                ws += 1
-            j -= 1
-    assert checked > 0, "no AGPR-accumulator MFMA found in the kernel assembly"
-    assert not problems, "\n".join(problems[:20])
 
 
 def test_no_packed_fp32_valu(asm_text):
@@ -210,6 +180,40 @@ def _in_flight_violations(code):
                 work.append((tgt, queue))
             i += 1
     return sorted(problems)
+
+
+def test_inline_asm_mfma_operands_settled(asm_text):
+    """Every inline-asm MFMA (the P V product, accumulating into AGPRs in the long instance and into
+    VGPRs in the short one) has no VALU write of one of its source registers within the two wait
+    states before it (the compiler pads only the MFMAs it emits itself)."""
+    checked, forms, problems = 0, set(), []
+    for name, code in _kernels(asm_text).items():
+        for i, (kind, s, from_asm) in enumerate(code):
+            if kind != "ins" or not from_asm or not s.startswith("v_mfma"):
+                continue
+            checked += 1
+            ops = _operands(s)
+            forms.add(ops[0][0])
+            srcs = _regs(ops[1]) | _regs(ops[2]) | _regs(ops[3])
+            ws, j = 0, i - 1
+            while j >= 0 and ws < WAIT_STATES:
+                k, t, _ = code[j]
+                if k == "label":
+                    problems.append(f"{name}: branch target within {WAIT_STATES} wait states of: {s}")
+                    break
+                if t.startswith("s_nop"):
+                    ws += int(t.split()[1]) + 1
+                else:
+                    op = t.split()[0]
+                    if op.startswith("v_") and not op.startswith("v_mfma") and " " in t:
+                        dst = t.split(None, 1)[1].split(",")[0].strip()
+                        if _regs(dst) & srcs:
+                            problems.append(f"{name}: {t}  ->  {s}")
+                    ws += 1
+                j -= 1
+    assert checked > 0, "no inline-asm MFMA found in the kernel assembly"
+    assert forms == {"a", "v"}, f"expected inline-asm MFMAs into AGPRs and into VGPRs, found {forms}"
+    assert not problems, "\n".join(problems[:20])
 
 
 @pytest.mark.parametrize("which", ["fused", "lbl"])
