@@ -7,9 +7,10 @@ Contents (all NumPy float64 or plain Python, no GPU):
 
 * :mod:`oracle.naive` -- the plain definition of scaled dot-product attention (Eq. 1): materialise
   the score matrix, mask, softmax, multiply by V. This is what the GPU path is checked against.
-* :mod:`oracle.tiled` -- a separately written online-softmax version following the per-tile
-  algorithm (Alg. 1) and the tile-to-tile split/merge (Alg. 2, with the merge read as the standard
-  log-sum-exp combination). Used to cross-check the naive oracle.
+* :mod:`oracle.tiled` -- a separately written streaming version built on the decomposition the
+  paper's per-tile (Alg. 1) and tile-to-tile (Alg. 2) algorithms rest on: per query row, the
+  attention over a key set and that set's log-sum-exp, folded over key chunks and key-range parts
+  (the log-sum-exp merge). Used to cross-check the naive oracle.
 * :mod:`oracle.brute` -- scalar double loops over Python floats with ``math.exp``, for tiny inputs.
 * :mod:`oracle.layer_by_layer` -- the paper's unfused layer-by-layer mapping as three operators with
   bfloat16 intermediates (score matrix, probabilities), the oracle of the unfused GPU baseline, with

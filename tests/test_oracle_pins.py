@@ -212,6 +212,41 @@ def test_tiled_matches_naive_with_empty_rows_and_parts():
     assert np.max(np.abs(l1[fin] - l2[fin])) < 1e-12
 
 
+def _planted_folds():
+    """Plausible mistakes in the streaming oracle's fold of two (A, Z) pairs."""
+    def no_rescale_running(a1, z1, a2, z2):  # forgets to rescale the running pair
+        z = np.logaddexp(z1, z2)
+        w2 = np.where(np.isfinite(z), np.exp(z2 - np.where(np.isfinite(z), z, 0.0)), 0.0)
+        return a1 + w2[:, None] * a2, z
+
+    def max_not_lse(a1, z1, a2, z2):  # keeps the larger log-sum-exp instead of their sum
+        z = np.maximum(z1, z2)
+        live = np.isfinite(z)
+        zs = np.where(live, z, 0.0)
+        return (np.where(live, np.exp(z1 - zs), 0.0)[:, None] * a1
+                + np.where(live, np.exp(z2 - zs), 0.0)[:, None] * a2), z
+
+    def swapped_weights(a1, z1, a2, z2):  # each side weighted by the other side's mass
+        z = np.logaddexp(z1, z2)
+        live = np.isfinite(z)
+        zs = np.where(live, z, 0.0)
+        return (np.where(live, np.exp(z2 - zs), 0.0)[:, None] * a1
+                + np.where(live, np.exp(z1 - zs), 0.0)[:, None] * a2), z
+    return [no_rescale_running, max_not_lse, swapped_weights]
+
+
+@pytest.mark.parametrize("bad", _planted_folds(), ids=lambda f: f.__name__)
+def test_tiled_pin_catches_planted_fold_mistakes(bad, monkeypatch):
+    """The tiled-vs-naive pin is not vacuous: each planted mistake in the fold makes it fail."""
+    import oracle.tiled as tiled
+
+    q, k, v = rnd(37, 9, scale=2.0), rnd(53, 9, scale=2.0), rnd(53, 7)
+    o1, l1 = attention_head(q, k, v, 0.55, False)
+    monkeypatch.setattr(tiled, "_fold", bad)
+    o2, l2 = tiled.spatial_flash_attention(q, k, v, 0.55, False, 16, 3, 2)
+    assert max(np.max(np.abs(o1 - o2)), np.max(np.abs(l1 - l2))) > 1e-6
+
+
 @pytest.mark.parametrize("Sq,Sk,causal", [(1, 1, False), (2, 3, False), (4, 4, True), (3, 2, True),
                                           (4, 2, False), (1, 4, True)])
 def test_brute_force_matches_naive(Sq, Sk, causal):
