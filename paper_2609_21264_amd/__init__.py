@@ -137,6 +137,20 @@ def fa_fwd_unfused(Q: int, K: int, V: int, O: int, LSE: Optional[int], B: int, H
                                           int(bool(causal)), workspace, int(workspace_bytes), stream))
 
 
+def _stream(stream, device):
+    """(torch stream, raw handle) for ``stream``: None is torch's current stream of ``device``; a
+    torch.cuda.Stream is used as is; a raw integer handle is wrapped in torch.cuda.ExternalStream so
+    that workspaces allocated for the call can be recorded on it (the caching allocator then does not
+    hand them out again before the kernels on that stream have run)."""
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    elif not isinstance(stream, torch.cuda.Stream):
+        stream = torch.cuda.ExternalStream(int(stream), device=device)
+    return stream, stream.cuda_stream
+
+
 def _check_qkv(q, k, v):
     import torch
 
@@ -171,15 +185,12 @@ def forward_unfused(q, k, v, causal: bool = False, scale: Optional[float] = None
         scale = 1.0 / math.sqrt(dqk)
     out = torch.empty((B, Hq, Sq, dv), dtype=torch.bfloat16, device=q.device)
     lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if return_lse else None
-    if stream is None:
-        stream = torch.cuda.current_stream(q.device)
-    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    stream, handle = _stream(stream, q.device)
     with torch.cuda.device(q.device):
         if workspace is None:
             nbytes = fa_lbl_workspace_bytes(B, Hq, Sq, Sk)
             workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
-            if isinstance(stream, torch.cuda.Stream):
-                workspace.record_stream(stream)
+            workspace.record_stream(stream)  # not reused before the kernels on `stream` ran
         st = fa_fwd_unfused(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                             lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, dqk, dv, scale, causal,
                             workspace.data_ptr(), workspace.numel() * workspace.element_size(), handle)
@@ -205,35 +216,25 @@ def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return
     """
     import torch
 
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        if not isinstance(t, torch.Tensor) or t.dim() != 4:
-            raise ValueError(f"{name} must be a 4-d torch tensor (BHSD)")
-        if t.dtype != torch.bfloat16:
-            raise ValueError(f"{name} must be bfloat16")
-        if not t.is_cuda:
-            raise ValueError(f"{name} must be on a GPU")
-        if not t.is_contiguous():
-            raise ValueError(f"{name} must be contiguous")
-    if not (q.device == k.device == v.device):
-        raise ValueError("q, k, v must be on the same device")
-    B, Hq, Sq, dqk = q.shape
-    Bk, Hkv, Sk, dk = k.shape
-    if Bk != B or dk != dqk or v.shape[:3] != k.shape[:3]:
-        raise ValueError(f"inconsistent shapes q{tuple(q.shape)} k{tuple(k.shape)} v{tuple(v.shape)}")
-    dv = v.shape[3]
+    B, Hq, Hkv, Sq, Sk, dqk, dv = _check_qkv(q, k, v)
     if scale is None:
         scale = 1.0 / math.sqrt(dqk)
     if out is None:
         out = torch.empty((B, Hq, Sq, dv), dtype=torch.bfloat16, device=q.device)
-    elif out.shape != (B, Hq, Sq, dv) or out.dtype != torch.bfloat16 or not out.is_contiguous():
+    elif (not isinstance(out, torch.Tensor) or out.shape != (B, Hq, Sq, dv) or out.dtype != torch.bfloat16
+          or not out.is_contiguous()):
         raise ValueError("out must be a contiguous bf16 tensor of shape [B, Hq, Sq, d_v]")
+    elif out.device != q.device:
+        raise ValueError(f"out must be on the inputs' device {q.device}, not {out.device}")
     if return_lse and lse is None:
         lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
-    if lse is not None and (lse.shape != (B, Hq, Sq) or lse.dtype != torch.float32 or not lse.is_contiguous()):
-        raise ValueError("lse must be a contiguous float32 tensor of shape [B, Hq, Sq]")
-    if stream is None:
-        stream = torch.cuda.current_stream(q.device)
-    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    if lse is not None:
+        if (not isinstance(lse, torch.Tensor) or lse.shape != (B, Hq, Sq) or lse.dtype != torch.float32
+                or not lse.is_contiguous()):
+            raise ValueError("lse must be a contiguous float32 tensor of shape [B, Hq, Sq]")
+        if lse.device != q.device:
+            raise ValueError(f"lse must be on the inputs' device {q.device}, not {lse.device}")
+    stream, handle = _stream(stream, q.device)
     name = "fa_fwd_ex"
     if decode:
         n_cu = torch.cuda.get_device_properties(q.device).multi_processor_count
@@ -241,8 +242,7 @@ def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return
         with torch.cuda.device(q.device):
             nbytes = fa_fwd_split_workspace_bytes(B, Hq, Sq, dv, parts)
             ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
-            if isinstance(stream, torch.cuda.Stream):
-                ws.record_stream(stream)
+            ws.record_stream(stream)
             st = fa_fwd_decode(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, dqk, dv, scale, causal,
                                parts, ws.data_ptr(), nbytes, handle)
@@ -259,8 +259,7 @@ def forward(q, k, v, causal: bool = False, scale: Optional[float] = None, return
             name = "fa_fwd_split"
             nbytes = fa_fwd_split_workspace_bytes(B, Hq, Sq, dv, int(n_split))
             ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
-            if isinstance(stream, torch.cuda.Stream):
-                ws.record_stream(stream)  # the caching allocator must not reuse it before the kernels ran
+            ws.record_stream(stream)  # the caching allocator must not reuse it before the kernels ran
             st = fa_fwd_split(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                               lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, dqk, dv, scale,
                               causal, int(n_split), ws.data_ptr(), nbytes, handle)

@@ -136,6 +136,25 @@ def test_python_forward_rejects_cpu_tensors(lib):
         fa.forward(q.float(), q, q)
 
 
+def test_python_forward_rejects_out_and_lse_on_another_device(lib, monkeypatch):
+    """out / lse on another device than q, k, v raise ValueError before any launch. The inputs here
+    are CPU tensors with the input check stubbed out (no GPU in this test); out / lse live on the
+    meta device, a device different from the inputs'."""
+    import torch
+
+    q = torch.zeros(1, 2, 8, 64, dtype=torch.bfloat16)
+    monkeypatch.setattr(fa, "_check_qkv", lambda q_, k_, v_: (1, 2, 2, 8, 8, 64, 64))
+    monkeypatch.setattr(fa, "fa_fwd_ex", lambda *a: pytest.fail("launched despite a bad out / lse"))
+    bad_out = torch.empty(1, 2, 8, 64, dtype=torch.bfloat16, device="meta")
+    with pytest.raises(ValueError, match="out must be on"):
+        fa.forward(q, q, q, out=bad_out)
+    bad_lse = torch.empty(1, 2, 8, dtype=torch.float32, device="meta")
+    with pytest.raises(ValueError, match="lse must be on"):
+        fa.forward(q, q, q, out=torch.empty_like(q), lse=bad_lse)
+    with pytest.raises(ValueError, match="out must be a contiguous"):
+        fa.forward(q, q, q, out=torch.empty(1, 2, 8, 64, dtype=torch.float32))
+
+
 # ---- split mode (fa_fwd_split): host-side checks only ----------------------------------------------
 
 WSP = P + 0x10000  # fake, 16-byte aligned workspace address

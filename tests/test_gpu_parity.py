@@ -225,3 +225,34 @@ def test_fa_fwd_entry_point():
     assert torch.equal(o1, o2)
     o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), to_f64(v), w.scale, w.causal)
     compare(to_f64(o1), lse.cpu().double().numpy(), o_ref, lse_ref, w.name)
+
+
+def test_forward_rejects_out_and_lse_on_the_host():
+    """A caller-supplied out or lse in host memory is rejected before any launch (its pointer would
+    otherwise reach the kernel)."""
+    w = _case("host out", dqk=128, dv=128, Hq=2, Hkv=1, Sq=64, Sk=64, seed=96)
+    q, k, v = (x.cuda() for x in W.make_inputs(w))
+    with pytest.raises(ValueError, match="out must be on"):
+        fa.forward(q, k, v, out=torch.empty(1, 2, 64, 128, dtype=torch.bfloat16))
+    with pytest.raises(ValueError, match="lse must be on"):
+        fa.forward(q, k, v, lse=torch.empty(1, 2, 64, dtype=torch.float32))
+
+
+def test_raw_stream_handle_keeps_the_split_workspace_alive():
+    """A raw stream handle (an int) is wrapped so that the split-mode workspace is recorded on it: the
+    result on a busy side stream equals the result on the current stream, bit for bit."""
+    w = _case("raw handle split", dqk=128, dv=128, Hq=4, Hkv=2, Sq=100, Sk=3000, causal=False, seed=97)
+    q, k, v = (x.cuda() for x in W.make_inputs(w))
+    ref = fa.forward(q, k, v, scale=w.scale, return_lse=True, n_split=4)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    outs = []
+    for _ in range(8):
+        outs.append(fa.forward(q, k, v, scale=w.scale, return_lse=True, n_split=4, stream=side.cuda_stream))
+        junk = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")  # reuses freed blocks at once
+        junk.fill_(0xff)
+    side.synchronize()
+    torch.cuda.synchronize()
+    for o, l in outs:
+        assert torch.equal(o, ref[0]) and torch.equal(l, ref[1])
