@@ -241,7 +241,8 @@ void fa_decode_kernel(DecodeParams p) {
         acc += wt[w] * *reinterpret_cast<const f32x4*>(ob + (w * 32 + col) * C::OROW + d0 + d);
       *reinterpret_cast<f32x4*>(dst + d) = acc * inv;
     }
-    if (tid % TPC == 0) p.lse_part[(int64_t)part * p.total_rows + orow_g] = L > 0.f ? (M + log2f(L)) * 0.69314718055994530942f : -INFINITY;
+    if (tid % TPC == 0)
+      p.lse_part[(int64_t)part * p.total_rows + orow_g] = L > 0.f ? (M + log2f(L)) * 0.69314718055994530942f : -INFINITY;
   }
 }
 

@@ -216,23 +216,12 @@ struct Attn {
   f32x16 oacc[DB][QB];
   float m_run[QB], l_run[QB];
 
-  // Slot order of a step: the P V MFMAs of tile j-1 first, then the score MFMAs of tile j+1. The
-  // exponentials of tile j run from slot E0 on, evenly spread: P V consumes the previous tile's P
-  // chunk c (16 keys) in slots [c*E0, (c+1)*E0), and chunk c of the new P is produced only after
-  // that, so both tiles' P share registers. The score accumulators of block kb+1 start after the
-  // exponentials of block kb of the previous scores (block-major order), so the two score tiles
-  // overlap in registers only partly.
+  // Slot order of a step: the P V MFMAs of tile j-1 first (chunk c of P, 16 keys, in slots
+  // [c * E0, (c + 1) * E0)), then the score MFMAs of tile j+1 (32-key-block-major, so that the score
+  // accumulators of block kb of the new tile are written only after the exponentials of block kb of
+  // the current one, and the two score tiles overlap in registers only partly).
   static constexpr int E0 = NMP / PS;
-  static_assert(NSL >= 5 * E0, "exponentials of chunk c must follow the P V MFMAs of chunk c");
-  static constexpr bool at_most_two_pairs_per_slot() {
-    for (int sl = 0; sl < NSL; ++sl)
-      if (exp_end(sl) - exp_begin(sl) > 2) return false;
-    return true;
-  }
   static constexpr bool slot_is_score(int sl) { return sl >= NMP; }
-  // exponential pairs of slot sl: u with E0 + floor(u * (NSL - E0) / NEP) == sl
-  static constexpr int exp_begin(int sl) { return sl < E0 ? 0 : ((sl - E0) * NEP + NSL - E0 - 1) / (NSL - E0); }
-  static constexpr int exp_end(int sl) { return sl < E0 ? 0 : ((sl - E0 + 1) * NEP + NSL - E0 - 1) / (NSL - E0); }
 
   __device__ __forceinline__ u32x4 kfrag(const unsigned char* sK, int ks, int kb) const {
     const int row = kb * 32 + perm32(i32);
@@ -293,27 +282,48 @@ struct Attn {
     return half_swap_max(m);
   }
 
-  // Exponential pair u of a tile: p = 2^(cs * s - m_ref), the lane's row sum, and the bf16 pair.
-  // In the step the pair is done in two halves in consecutive slots: exp_first (2 fma, 2 exp) and
-  // exp_second (2 add, 1 pack), which keeps every slot's VALU work below one MFMA.
-  __device__ __forceinline__ f32x2 exp_first(int u, const Scores& cur, const float (&mref)[QB]) const {
-    const int qb = u % QB, rp = (u / QB) % 8, kb = u / (QB * 8);
-    f32x2 e = {__builtin_amdgcn_exp2f(fmaf(cur[kb][qb][2 * rp], cs, -mref[qb])),
-               __builtin_amdgcn_exp2f(fmaf(cur[kb][qb][2 * rp + 1], cs, -mref[qb]))};
-    asm volatile("" : "+v"(e));
-    return e;
+  // Element schedule of the step: the NEL = 2 * NEP exponentials of a tile are spread
+  // one by one over the NSL MFMA slots (element e in slot e * NSL / NEL), each as one fma and one
+  // exp2 right after the slot's MFMA; the two adds and the pack of pair u follow in the slot after
+  // the one of its second element. At d = 128 a slot then carries 3 and 6 full-rate-equivalent VALU
+  // instructions in turn, within what a 32-cycle MFMA absorbs. A pair's pack writes P chunk c only
+  // after the P V MFMAs of chunk c (slots [c * E0, (c + 1) * E0)) for every c >= 1, so the old and new
+  // P share registers there; chunk 0 is written earlier and takes registers of its own.
+  static constexpr int NEL = 2 * NEP;
+  static constexpr int elem_begin(int sl) { return (sl * NEL + NSL - 1) / NSL; }
+  static constexpr int elem_end(int sl) { return ((sl + 1) * NEL + NSL - 1) / NSL; }
+  static constexpr bool packs_follow_pv() {
+    for (int u = 0; u < NEP; ++u) {
+      int sl = 0;
+      while (elem_end(sl) <= 2 * u + 1) ++sl;  // slot of element 2u+1
+      const int c = u / (QB * 4);             // P chunk (16 keys) of pair u
+      if (c >= 1 && sl + 1 < (c + 1) * E0) return false;
+    }
+    return true;
   }
-  __device__ __forceinline__ void exp_second(int u, f32x2 e, Probs& pk, float (&rs)[QB]) const {
+  static_assert(packs_follow_pv(), "a pack would overwrite P of a chunk before its P V MFMAs");
+  static constexpr bool at_most_two_elems_per_slot() {
+    for (int sl = 0; sl < NSL; ++sl)
+      if (elem_end(sl) - elem_begin(sl) > 2) return false;
+    return true;
+  }
+
+  // Element e of a tile: p = 2^(cs * s - m_ref).
+  __device__ __forceinline__ float exp_elem(int e, const Scores& cur, const float (&mref)[QB]) const {
+    const int u = e >> 1, qb = u % QB, rp = (u / QB) % 8, kb = u / (QB * 8);
+    float x = __builtin_amdgcn_exp2f(fmaf(cur[kb][qb][2 * rp + (e & 1)], cs, -mref[qb]));
+    asm volatile("" : "+v"(x));
+    return x;
+  }
+  // Pair u: the lane's row sum and the bf16 pair. The first pair of each row block starts the sum.
+  __device__ __forceinline__ void pack_pair(int u, float e0, float e1, Probs& pk, float (&rs)[QB]) const {
     const int qb = u % QB, rp = (u / QB) % 8, kb = u / (QB * 8);
-    rs[qb] += e.x + e.y;
-    pk[kb][qb][rp] = pack_bf16x2(e.x, e.y);
-    // Keep the pack here: otherwise it is sunk past the rebase branch, which keeps both fp32
-    // exponentials alive across the whole step.
+    if (u < QB)
+      rs[qb] = e0 + e1;
+    else
+      rs[qb] += e0 + e1;
+    pk[kb][qb][rp] = pack_bf16x2(e0, e1);
     asm volatile("" : "+v"(pk[kb][qb][rp]));
-  }
-  __device__ __forceinline__ void exp_pair(int u, const Scores& cur, Probs& pk, const float (&mref)[QB],
-                                           float (&rs)[QB]) const {
-    exp_second(u, exp_first(u, cur, mref), pk, rs);
   }
 
   // P V MFMA number p of a tile (order ps, db, qb), V fragments read VPF ahead. `settled`: P was
@@ -372,10 +382,12 @@ struct Attn {
         agpr_fence<AG>(oacc[db][qb]);
       }
       mref[qb] = m_new == -INFINITY ? 0.f : m_new;
-      rs[qb] = 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < NEP; ++u) exp_pair(u, cur, pk, mref, rs);
+    for (int u = 0; u < NEP; ++u) {
+      const float e0 = exp_elem(2 * u, cur, mref), e1 = exp_elem(2 * u + 1, cur, mref);
+      pack_pair(u, e0, e1, pk, rs);
+    }
   }
 
   // One pipeline step: P V of tile j-1 (pk_old, V slot sVo), exponentials of tile j (cur, key n0,
@@ -399,8 +411,8 @@ struct Attn {
     bf16x8 vf[NVF];
 #pragma unroll
     for (int t = 0; t < VPF && t < NVF; ++t) vf[t] = vfrag(sVo, t / DB, t % DB);
-    static_assert(at_most_two_pairs_per_slot(), "ehalf holds the first halves of two slots");
-    f32x2 ehalf[4];  // first halves in flight
+    static_assert(at_most_two_elems_per_slot(), "ev holds the elements of two slots");
+    float ev[4];  // exponentials in flight, element e in ev[e % 4]
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
@@ -413,17 +425,19 @@ struct Attn {
         score_mfma(nxt, kf, sKn, sl - NMP);
       else
         pv_mfma(sl, pk_old, vf, sVo, true);
-      // second halves of the previous slot's pairs, first halves of this slot's pairs
+      __builtin_amdgcn_sched_barrier(0);  // the slot's MFMA is issued before its VALU work
       if (sl > 0) {
 #pragma unroll
-        for (int u = exp_begin(sl - 1); u < exp_end(sl - 1); ++u) exp_second(u, ehalf[u % 4], pk_new, rs);
+        for (int e = elem_begin(sl - 1); e < elem_end(sl - 1); ++e)
+          if (e & 1) pack_pair(e >> 1, ev[(e - 1) % 4], ev[e % 4], pk_new, rs);
       }
 #pragma unroll
-      for (int u = exp_begin(sl); u < exp_end(sl); ++u) ehalf[u % 4] = exp_first(u, cur, mref);
+      for (int e = elem_begin(sl); e < elem_end(sl); ++e) ev[e % 4] = exp_elem(e, cur, mref);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
-    for (int u = exp_begin(NSL - 1); u < exp_end(NSL - 1); ++u) exp_second(u, ehalf[u % 4], pk_new, rs);
+    for (int e = elem_begin(NSL - 1); e < elem_end(NSL - 1); ++e)
+      if (e & 1) pack_pair(e >> 1, ev[(e - 1) % 4], ev[e % 4], pk_new, rs);
     bool over = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) over = over || !(rs[qb] <= kOverflowSum);
