@@ -87,3 +87,12 @@ def test_short_instance_runs_the_small_benchmark_configs(cfg):
     w = W.CONFIGS[cfg]
     assert blocks(w) <= SHORT_MAX_BLOCKS
     check_full(w.with_(seed=w.seed + 700))
+
+
+@pytest.mark.parametrize("heads", [256, 257], ids=["256-blocks-short", "257-blocks-long"])
+def test_instance_boundary(heads):
+    """Either side of the switch between the instances: 256 blocks (short) and 257 (long)."""
+    w = W.small(f"boundary {heads}", Hq=heads, Hkv=heads, Sq=100, Sk=150, causal=True, seed=191)
+    assert blocks(w) == heads
+    print(f"\n[case] {w}", flush=True)
+    check_full(w)

@@ -7,7 +7,8 @@ every head), K = 0 except the last key K[L] = (s_h / scale) e0 with a score s_h 
 key/value head h, V = a except V[L] = b. A query row that sees the keys 0 .. n-1 (n <= L) gets O = a
 and LSE = ln n; a row that also sees key L gets O = (L a + e^s b) / (L + e^s) and LSE = ln(L + e^s).
 The last key's score sits far above the others, so the fused kernel's online softmax must rebase on
-the last tile. Two query heads share each key/value head (grouped-query attention).
+the last tile. Two query heads share each key/value head (grouped-query attention); a second fused
+run with 129 per key/value head has enough query blocks for the long kernel instance.
 """
 
 import math
@@ -30,8 +31,8 @@ MAX_SK = (2 ** 31 - 1) // D // 64 * 64        # largest Sk with Sk * d < 2^31, a
 LBL_MAX_SK = 2 ** 22                          # the layer-by-layer operators' limit
 
 
-def spike_inputs(sq, sk, hkv):
-    q = torch.zeros(1, hkv * GROUP, sq, D, dtype=torch.bfloat16, device="cuda")
+def spike_inputs(sq, sk, hkv, group=GROUP):
+    q = torch.zeros(1, hkv * group, sq, D, dtype=torch.bfloat16, device="cuda")
     q[..., 0] = 1.0
     k = torch.zeros(1, hkv, sk, D, dtype=torch.bfloat16, device="cuda")
     for h in range(hkv):
@@ -55,10 +56,10 @@ def expected(sq, sk, causal, spike):
     return o, lse
 
 
-def check(o, lse, sq, sk, causal, what):
+def check(o, lse, sq, sk, causal, what, group=GROUP):
     got_o, got_lse = to_f64(o.cpu())[0], lse.cpu().double().numpy()[0]
     for hq in range(got_o.shape[0]):
-        o_ref, lse_ref = expected(sq, sk, causal, SPIKES[hq // GROUP])
+        o_ref, lse_ref = expected(sq, sk, causal, SPIKES[hq // group])
         # one bf16 rounding of O plus fp32 accumulation over Sk terms; the bar of the prefill kernel
         assert np.all(np.abs(got_o[hq] - o_ref[:, None]) <= 2e-2), f"{what} head {hq}: {got_o[hq, :, 0]} vs {o_ref}"
         assert np.abs(got_lse[hq] - lse_ref).max() <= 1e-3, f"{what} head {hq}: LSE {got_lse[hq]} vs {lse_ref}"
@@ -79,6 +80,20 @@ def test_fused_at_largest_key_length(big, causal):
     o, lse = fa.forward(q, k, v, causal=causal, scale=SCALE, return_lse=True)
     torch.cuda.synchronize()
     check(o, lse, sq, MAX_SK, causal, f"fused causal={causal}")
+
+
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_fused_long_instance_at_largest_key_length(big, causal):
+    """The same keys with 129 query heads per key/value head: 258 query blocks, more than the short
+    instance takes, so the long instance's loaders address the end of the 4 GiB heads."""
+    sq, _, k, v = big
+    group = 129
+    assert 2 * group * -(-sq // fa.fa_block_rows(D, D, causal)) > 256
+    q = torch.zeros(1, 2 * group, sq, D, dtype=torch.bfloat16, device="cuda")
+    q[..., 0] = 1.0
+    o, lse = fa.forward(q, k, v, causal=causal, scale=SCALE, return_lse=True)
+    torch.cuda.synchronize()
+    check(o, lse, sq, MAX_SK, causal, f"fused long causal={causal}", group)
 
 
 def test_split_at_largest_key_length(big):
