@@ -730,8 +730,10 @@ void fa_fwd_kernel(FwdParams p) {
 // and P in VGPRs) is what fixes 64 query rows per wave. K tiles are loaded two ahead: a third K slot
 // measured 2-3 % slower on the 8K, 4K-d192 and 128K prefill shapes (one box, interleaved).
 // Short: 4 waves x 32 query rows (128 rows per workgroup), two workgroups per CU (two waves per SIMD,
-// 256 registers each, O and Q in VGPRs), a 3-slot V ring so that two rings fit one CU's LDS, and
-// shallower fragment prefetch at d = 128 so that the step fits the registers without spilling. It
+// 256 registers each, O and Q in VGPRs), shallower fragment prefetch at d = 128 so that the step fits
+// the registers without spilling, and a V ring of 3 slots at d = 128 (so that two rings fit one CU's
+// LDS) and 4 at d = 64 (V tiles loaded two steps ahead; 3-8 % faster than 3 slots on the d = 64
+// shapes it runs, while a deeper K ring measured slower). It
 // runs problems with few query blocks (short sequences, few heads), where 256-row blocks leave CUs
 // idle and each block's serial chain of steps sets the time: on the paper's S = 512 and 2048 GPT-2
 // and BERT shapes and the 128K single-head workload it measured 1.2-1.4x faster than the long
@@ -765,7 +767,7 @@ struct Instance {
 };
 template <int DQK, int DV, bool CAUSAL>
 struct ShortInstance {
-  using C = Cfg<DQK, DV, 64, 4, 1, CAUSAL, false, 2, DQK >= 128 ? 1 : 2, DQK >= 128 ? 2 : 6, 2, 3>;
+  using C = Cfg<DQK, DV, 64, 4, 1, CAUSAL, false, 2, DQK >= 128 ? 1 : 2, DQK >= 128 ? 2 : 6, 2, DQK >= 128 ? 3 : 4>;
 };
 
 // Largest grid of long-instance workgroups (256-row blocks) that runs the short instance instead:
