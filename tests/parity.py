@@ -12,7 +12,7 @@ import torch
 
 import paper_2609_21264_amd as fa
 import workloads as W
-from oracle import bf16_bits_to_f64, naive_attention, naive_attention_rows
+from oracle import attention_head, bf16_bits_to_f64, naive_attention, naive_attention_rows
 
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
@@ -62,6 +62,34 @@ def check_full(w: W.Workload, device="cuda:0"):
     o, lse = run_gpu(q, k, v, w, device)
     o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), to_f64(v), w.scale, w.causal)
     return compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name, max(1.0, w.sigma))
+
+
+def check_every_element(w: W.Workload, device="cuda:0", workers: int = 8):
+    """Every output element of a large workload against the naive oracle, head by head.
+
+    The oracle materialises each head's full score matrix (512 MiB in float64 at 8192 x 8192), so
+    heads run ``workers`` at a time in threads (NumPy releases the GIL in its array kernels); the
+    result is the same comparison as :func:`check_full`."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    q, k, v = W.make_inputs(w)
+    o, lse = run_gpu(q, k, v, w, device)
+    o_gpu, lse_gpu = to_f64(o), lse.cpu().double().numpy()
+    o_ref = np.empty_like(o_gpu)
+    lse_ref = np.empty_like(lse_gpu)
+    group = w.Hq // w.Hkv
+
+    def head(bh):
+        b, h = divmod(bh, w.Hq)
+        o_ref[b, h], lse_ref[b, h] = attention_head(to_f64(q[b, h]), to_f64(k[b, h // group]),
+                                                    to_f64(v[b, h // group]), w.scale, w.causal)
+        return bh
+
+    with ThreadPoolExecutor(max_workers=workers) as pool:
+        for n, _ in enumerate(pool.map(head, range(w.B * w.Hq)), 1):
+            if n % 16 == 0:
+                print(f"[oracle] {n} of {w.B * w.Hq} heads", flush=True)
+    return compare(o_gpu, lse_gpu, o_ref, lse_ref, w.name, max(1.0, w.sigma))
 
 
 def check_rows(w: W.Workload, rows_per_head: int, device="cuda:0", inputs=None):

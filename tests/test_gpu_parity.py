@@ -11,7 +11,7 @@ import torch
 
 import paper_2609_21264_amd as fa
 import workloads as W
-from parity import check_full, check_rows, compare, run_gpu, to_f64
+from parity import check_every_element, check_full, check_rows, compare, run_gpu, to_f64
 from oracle import naive_attention
 
 pytestmark = pytest.mark.gpu
@@ -56,6 +56,13 @@ def test_benchmark_config_full(cfg):
     w = W.CONFIGS[cfg]
     print(f"\n[case] config {cfg}: {w}", flush=True)
     check_full(w)
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_benchmark_config_every_element(cfg):
+    w = W.CONFIGS[cfg]
+    print(f"\n[case] config {cfg}, every element: {w}", flush=True)
+    check_every_element(w)
 
 
 @pytest.mark.parametrize("cfg,rows", [(3, 256), (4, 128), (5, 64)])
