@@ -148,6 +148,8 @@ def _stream(stream, device):
         stream = torch.cuda.current_stream(device)
     elif not isinstance(stream, torch.cuda.Stream):
         stream = torch.cuda.ExternalStream(int(stream), device=device)
+    elif stream.device != torch.device(device):
+        raise ValueError(f"stream is on {stream.device}, the tensors on {device}")
     return stream, stream.cuda_stream
 
 

@@ -245,6 +245,14 @@ def test_forward_rejects_out_and_lse_on_the_host():
         fa.forward(q, k, v, lse=torch.empty(1, 2, 64, dtype=torch.float32))
 
 
+def test_stream_on_another_device_is_rejected():
+    # a torch stream must belong to the tensors' device (the kernels run on the stream's device)
+    s = torch.cuda.Stream()
+    with pytest.raises(ValueError, match="stream is on"):
+        fa._stream(s, torch.device("cpu"))
+    assert fa._stream(s, s.device)[1] == s.cuda_stream
+
+
 def test_raw_stream_handle_keeps_the_split_workspace_alive():
     """A raw stream handle (an int) is wrapped so that the split-mode workspace is recorded on it: the
     result on a busy side stream equals the result on the current stream, bit for bit."""
