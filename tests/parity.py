@@ -32,12 +32,13 @@ def run_gpu(q, k, v, w: W.Workload, device="cuda:0", stream=None):
 
 
 def compare(o_gpu: np.ndarray, lse_gpu: np.ndarray, o_ref: np.ndarray, lse_ref: np.ndarray, what="",
-            v_scale: float = 1.0):
+            v_scale: float = 1.0, o_bar=None):
     """Assert the acceptance bar; returns (max_abs, mean_abs, lse_max).
 
     The output bars are stated for unit-variance inputs. O is linear in V, so for inputs whose values
     are drawn with standard deviation sigma the O bars scale by ``v_scale = max(1, sigma)``; the LSE
-    bar does not depend on V.
+    bar does not depend on V. ``o_bar`` (an array broadcastable to O, see :func:`rounding_bar`)
+    replaces the max-abs bar with a per-element one.
     """
     assert o_gpu.shape == o_ref.shape, (o_gpu.shape, o_ref.shape)
     assert np.all(np.isfinite(o_gpu)), f"{what}: non-finite output"
@@ -48,12 +49,29 @@ def compare(o_gpu: np.ndarray, lse_gpu: np.ndarray, o_ref: np.ndarray, lse_ref: 
     assert np.array_equal(np.isneginf(lse_gpu), empty_ref), f"{what}: -inf LSE rows differ"
     fin = ~empty_ref
     lse_max = float(np.abs(lse_gpu[fin] - lse_ref[fin]).max()) if fin.any() else 0.0
-    assert max_abs <= MAX_ABS * v_scale, f"{what}: max-abs {max_abs:.3e}"
+    if o_bar is None:
+        assert max_abs <= MAX_ABS * v_scale, f"{what}: max-abs {max_abs:.3e}"
+    else:
+        worst = float((err / o_bar).max()) if err.size else 0.0
+        assert worst <= 1.0, f"{what}: max-abs {max_abs:.3e}, {worst:.3f} of the per-element bar"
     assert mean_abs <= MEAN_ABS * v_scale, f"{what}: mean-abs {mean_abs:.3e}"
     assert lse_max <= LSE_ABS, f"{what}: LSE max-abs {lse_max:.3e}"
     if empty_ref.any():
         assert np.all(o_gpu[empty_ref] == 0.0), f"{what}: rows with no visible key must be 0"
     return max_abs, mean_abs, lse_max
+
+
+def rounding_bar(v: np.ndarray, hq: int) -> np.ndarray:
+    """Max-abs bar on O derived from the arithmetic, for inputs that are not unit-variance: bf16 keeps
+    8 significant bits (unit roundoff u = 2^-8); P enters the P V product rounded to bf16 (at most
+    u max|V| on O, a convex combination of V rows) and O is rounded to bf16 once (at most u |O| <=
+    u max|V|), while fp32 accumulation and v_exp_f32 add ~1e-6 relative. So |O - O_ref| <= 2^-7 max|V|
+    of the head's key/value rows. As the softmax sharpens (larger sigma) O approaches single V rows,
+    which the unit-variance bar scaled by sigma does not follow. Returns [B, Hq, 1, 1] from v
+    [B, Hkv, Sk, dv] (float64)."""
+    vmax = np.abs(v).max(axis=(2, 3)) if v.size else np.zeros(v.shape[:2])
+    g = hq // v.shape[1]
+    return (2.0 ** -7 * np.repeat(vmax, g, axis=1) + 1e-6)[:, :, None, None]
 
 
 def check_full(w: W.Workload, device="cuda:0"):

@@ -13,7 +13,7 @@ import pytest
 
 import workloads as W
 from oracle import naive_attention
-from parity import check_rows, run_gpu, to_f64
+from parity import check_rows, rounding_bar, run_gpu, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -46,8 +46,7 @@ def test_sigma_sweep(sigma):
     err = np.abs(og - o_ref)
     mae = float(err.mean())
     rho = [float(np.corrcoef(og[0, h].ravel(), o_ref[0, h].ravel())[0, 1]) for h in range(w.Hq)]
-    vmax = np.abs(vf).max(axis=(2, 3))  # [B, H]
-    ratio = float((err.max(axis=(2, 3)) / (2.0 ** -7 * vmax + 1e-6)).max())
+    ratio = float((err / rounding_bar(vf, w.Hq)).max())
     lse_err = float(np.abs(lse.cpu().double().numpy() - lse_ref).max())
     print(f"\n[sigma sweep] sigma {sigma}: MAE {mae:.3e} (paper {PAPER_MAE[sigma]:.1e}), min per-head Pearson "
           f"{min(rho):.7f}, max-abs / (2^-7 max|V|) {ratio:.3f}, LSE max-abs {lse_err:.2e}")
