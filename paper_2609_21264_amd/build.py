@@ -44,6 +44,9 @@ def _device_flags() -> list:
         # The pipelined step is one fully unrolled sequence of MFMA slots; the default limit for
         # "#pragma unroll" stops short of it for the widest head dimension.
         "-mllvm", "-pragma-unroll-threshold=50000",
+        # Leading scalar kernel arguments (up to 14 SGPRs) are preloaded by the command processor, so
+        # that the fused kernel's first loads do not wait for the argument block.
+        "-mllvm", "-amdgpu-kernarg-preload-count=14",
         "-I", INCLUDE, "-I", CSRC,
     ]
 

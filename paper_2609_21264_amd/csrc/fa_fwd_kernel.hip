@@ -154,28 +154,54 @@ struct Cfg {
   static_assert(LDS_BYTES * OCC_ <= 163840, "LDS budget of the workgroups sharing a CU");
 };
 
-// Map a hardware workgroup index to (batch, query head, query block). Workgroup t runs on XCD
-// t % 8. Logical work items are ordered heaviest query block first (causal), then batch, key/value
-// head and group member; each group of `group` consecutive items (the query heads of one key/value
-// head at one query block) is placed on one XCD, and groups go to XCDs round-robin.
-__device__ __forceinline__ void decode_workgroup(int t, const FwdParams& p, bool causal, int& b, int& hq,
-                                                 int& qtile) {
-  const int G = p.group;
-  const int span = kNumXcd * G;
-  const int full = (p.n_wg / span) * span;
-  int L = t;
-  if (t < full) {
-    const int xcd = t % kNumXcd, slot = t / kNumXcd;
-    L = ((slot / G) * kNumXcd + xcd) * G + slot % G;
+// Division by a divisor that is fixed for the launch, as a multiply-high and two shifts (Granlund and
+// Montgomery, "Division by invariant integers using multiplication", PLDI 1994, the algorithm for
+// unsigned 32-bit operands): with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1, every 32-bit
+// n has n / d = (t + ((n - t) >> min(l, 1))) >> max(l - 1, 0), t = mulhi(m, n). The host computes m and
+// the two shifts (6 bits: min(l, 1) | max(l - 1, 0) << 1); the kernel's work decomposition then needs
+// no division sequence (a runtime division by a value the compiler cannot see is ~25 instructions).
+struct FastDiv {
+  uint32_t m, sh;
+};
+FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((uint64_t{1} << l) < d) ++l;
+  const uint64_t m = ((uint64_t{1} << 32) * ((uint64_t{1} << l) - d)) / d + 1;
+  return {static_cast<uint32_t>(m), (l < 1 ? l : 1u) | ((l > 0 ? l - 1 : 0u) << 1)};
+}
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t m, uint32_t sh) {
+  const uint32_t t = __umulhi(m, n);
+  return (t + ((n - t) >> (sh & 1u))) >> (sh >> 1);
+}
+
+// What the work decomposition needs, all uniform over the launch: group size, key/value heads,
+// batch, query blocks per head, the items in whole XCD spans (below), and the fast divisions by the
+// group size, the key/value heads and the batch (their shifts packed 6 bits apart).
+struct WorkMap {
+  int group, hkv, batch, n_qtiles, full;
+  uint32_t m_group, m_hkv, m_batch, shifts;
+};
+
+// Map a hardware workgroup index to (batch, key/value head, group member, query block). Workgroup t
+// runs on XCD t % 8. Logical work items are ordered heaviest query block first (causal), then batch,
+// key/value head and group member; each group of `group` consecutive items (the query heads of one
+// key/value head at one query block) is placed on one XCD, and groups go to XCDs round-robin
+// (`full` = the items in whole spans of 8 groups; the rest keep their order).
+__device__ __forceinline__ void decode_workgroup(uint32_t t, const WorkMap& w, bool causal, int& b, int& kvh,
+                                                 int& member, int& qtile) {
+  const uint32_t G = w.group, sg = w.shifts & 63u, sh = (w.shifts >> 6) & 63u, sb = (w.shifts >> 12) & 63u;
+  uint32_t L = t;
+  if (t < (uint32_t)w.full) {
+    const uint32_t xcd = t % kNumXcd, slot = t / kNumXcd, sq = fast_div(slot, w.m_group, sg);
+    L = (sq * kNumXcd + xcd) * G + (slot - sq * G);
   }
-  const int member = L % G;
-  int r = L / G;
-  const int kvh = r % p.hkv;
-  r /= p.hkv;
-  b = r % p.batch;
-  const int qt = r / p.batch;
-  qtile = causal ? p.n_qtiles - 1 - qt : qt;
-  hq = kvh * G + member;
+  uint32_t r = fast_div(L, w.m_group, sg);
+  member = (int)(L - r * G);
+  const uint32_t r2 = fast_div(r, w.m_hkv, sh);
+  kvh = (int)(r - r2 * (uint32_t)w.hkv);
+  const uint32_t qt = fast_div(r2, w.m_batch, sb);
+  b = (int)(r2 - qt * (uint32_t)w.batch);
+  qtile = causal ? w.n_qtiles - 1 - (int)qt : (int)qt;
 }
 
 // Per-wave state and the math of the pipelined step.
@@ -449,7 +475,21 @@ struct Attn {
 
 template <class C>
 __global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(C::WPE, C::WPE)))
-void fa_fwd_kernel(FwdParams p) {
+void fa_fwd_kernel(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, int a_batch, int a_hkv, int a_group, int a_nqt,
+                   int a_full, uint32_t a_mg, uint32_t a_mh, uint32_t a_mb, uint32_t a_shifts, FwdParams p) {
+  // The values the prologue needs first arrive as separate scalar arguments, which the command
+  // processor preloads into SGPRs before the first instruction (kernel-argument preloading, enabled at
+  // build time for the first 14 SGPRs of arguments); the rest of p is read from the argument block
+  // while the first loads are in flight.
+  p.q = a_q;
+  p.sq = a_sq;
+  p.sk = a_sk;
+  p.hq = a_hq;
+  p.batch = a_batch;
+  p.hkv = a_hkv;
+  p.group = a_group;
+  p.n_qtiles = a_nqt;
+  const WorkMap wm{a_group, a_hkv, a_batch, a_nqt, a_full, a_mg, a_mh, a_mb, a_shifts};
   using A = Attn<C>;
   constexpr int DQK = C::DQK, DV = C::DV, BN = C::BN, QB = C::QB;
 
@@ -466,19 +506,14 @@ void fa_fwd_kernel(FwdParams p) {
   st.v_key = 8 * (lane >> 5) + ((lane & 15) >> 2);                             // key in the 16-key step
   st.v_t = (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) ^ v_swizzle<DV>(st.v_key);  // low chunk bits, swizzled
   st.v_half = (lane & 1) * 8;                                                  // byte offset in the chunk
-  st.cs = p.cs;
-  st.mask_val = p.cs < 0.f ? INFINITY : -INFINITY;
   st.sk = p.sk;
 
   // Split mode: workgroup t takes part t / n_wg of work item t % n_wg.
   const int split = C::SPLIT ? (int)(blockIdx.x / p.n_wg) : 0;
-  int b, hq, qtile;
-  decode_workgroup(C::SPLIT ? (int)(blockIdx.x % p.n_wg) : (int)blockIdx.x, p, C::CAUSAL, b, hq, qtile);
-  const int g = hq / p.group;
+  int b, g, member, qtile;
+  decode_workgroup(C::SPLIT ? blockIdx.x % (uint32_t)p.n_wg : blockIdx.x, wm, C::CAUSAL, b, g, member, qtile);
+  const int hq = g * p.group + member;
   const uint16_t* __restrict__ qh = p.q + (size_t)(b * p.hq + hq) * p.sq * DQK;
-  const uint16_t* __restrict__ kh = p.k + (size_t)(b * p.hkv + g) * p.sk * DQK;
-  const uint16_t* __restrict__ vh = p.v + (size_t)(b * p.hkv + g) * p.sk * DV;
-  st.kg = kh;
 
   const int q0 = qtile * C::BM;
   st.qw = q0 + wave * 32 * QB;  // first query row of this wave
@@ -512,6 +547,12 @@ void fa_fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int ks = 0; ks < A::KS; ++ks) load_q<A::AG>(st.qf[qb][ks], qh + (size_t)row * DQK + ks * 16 + st.h * 8);
   }
+  // What comes from the argument block (not preloaded) is used only from here on.
+  const uint16_t* __restrict__ kh = p.k + (size_t)(b * p.hkv + g) * p.sk * DQK;
+  const uint16_t* __restrict__ vh = p.v + (size_t)(b * p.hkv + g) * p.sk * DV;
+  st.kg = kh;
+  st.cs = p.cs;
+  st.mask_val = p.cs < 0.f ? INFINITY : -INFINITY;
 
   // Rings: step j loads K(j+KA) and V(j+VA) (the group of step j); the prologue loads the groups of
   // j = -KA .. -1 (with the defaults KA = VA = 2: K0, V0, K1, V1 in this order), each group's V tile
@@ -785,7 +826,12 @@ template <class C>
 hipError_t launch_cfg(FwdParams p, hipStream_t stream) {
   p.n_qtiles = (p.sq + C::BM - 1) / C::BM;
   p.n_wg = p.batch * p.hq * p.n_qtiles;
-  void* args[] = {&p};
+  const int span = kNumXcd * p.group;
+  int full = (p.n_wg / span) * span;
+  FastDiv fg = make_fastdiv(p.group), fh = make_fastdiv(p.hkv), fb = make_fastdiv(p.batch);
+  uint32_t shifts = fg.sh | fh.sh << 6 | fb.sh << 12;
+  void* args[] = {&p.q,  &p.sq, &p.sk, &p.hq, &p.batch, &p.hkv, &p.group, &p.n_qtiles,
+                  &full, &fg.m, &fh.m, &fb.m, &shifts,  &p};
   return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel<C>), dim3(p.n_wg * (C::SPLIT ? p.n_split : 1)),
                          dim3(C::NT), args, 0, stream);
 }
