@@ -123,6 +123,7 @@ template <int DQK_, int DV_, int BN_, int NWAVES_, int QB_, bool CAUSAL_, bool S
 struct Cfg {
   static constexpr int DQK = DQK_, DV = DV_, BN = BN_, NWAVES = NWAVES_, QB = QB_;
   static constexpr int KPF = KPF_, VPF = VPF_;
+  static constexpr int OCC = OCC_;  // workgroups sharing a CU
   static constexpr bool CAUSAL = CAUSAL_;
   // SPLIT: each workgroup takes one of n_split contiguous parts of its query block's key tiles and
   // writes a partial result (O normalised by its own row sum, fp32, and its LSE) for a merge pass.
@@ -186,21 +187,28 @@ struct WorkMap {
 // runs on XCD t % 8. Logical work items are ordered heaviest query block first (causal), then batch,
 // key/value head and group member; each group of `group` consecutive items (the query heads of one
 // key/value head at one query block) is placed on one XCD, and groups go to XCDs round-robin
-// (`full` = the items in whole spans of 8 groups; the rest keep their order).
+// (`full` = the items in whole spans of 8 groups; the rest keep their order). FAST divides through
+// the multiply-high constants, else with the compiler's division sequence (the long instance: there
+// the faster prologue measured no gain in time, and on the 128K workload it shifted the relative
+// start times of the workgroups that stream one K/V head through an XCD's L2 enough to double the L2
+// misses; the mapping is the same either way).
+template <bool FAST>
 __device__ __forceinline__ void decode_workgroup(uint32_t t, const WorkMap& w, bool causal, int& b, int& kvh,
                                                  int& member, int& qtile) {
-  const uint32_t G = w.group, sg = w.shifts & 63u, sh = (w.shifts >> 6) & 63u, sb = (w.shifts >> 12) & 63u;
+  const uint32_t G = w.group, H = w.hkv, Bt = w.batch;
+  auto div = [&](uint32_t n, uint32_t d, uint32_t m, uint32_t s) { return FAST ? fast_div(n, m, s) : n / d; };
+  const uint32_t sg = w.shifts & 63u, sh = (w.shifts >> 6) & 63u, sb = (w.shifts >> 12) & 63u;
   uint32_t L = t;
   if (t < (uint32_t)w.full) {
-    const uint32_t xcd = t % kNumXcd, slot = t / kNumXcd, sq = fast_div(slot, w.m_group, sg);
+    const uint32_t xcd = t % kNumXcd, slot = t / kNumXcd, sq = div(slot, G, w.m_group, sg);
     L = (sq * kNumXcd + xcd) * G + (slot - sq * G);
   }
-  uint32_t r = fast_div(L, w.m_group, sg);
+  const uint32_t r = div(L, G, w.m_group, sg);
   member = (int)(L - r * G);
-  const uint32_t r2 = fast_div(r, w.m_hkv, sh);
-  kvh = (int)(r - r2 * (uint32_t)w.hkv);
-  const uint32_t qt = fast_div(r2, w.m_batch, sb);
-  b = (int)(r2 - qt * (uint32_t)w.batch);
+  const uint32_t r2 = div(r, H, w.m_hkv, sh);
+  kvh = (int)(r - r2 * H);
+  const uint32_t qt = div(r2, Bt, w.m_batch, sb);
+  b = (int)(r2 - qt * Bt);
   qtile = causal ? w.n_qtiles - 1 - (int)qt : (int)qt;
 }
 
@@ -473,23 +481,9 @@ struct Attn {
   }
 };
 
+// The kernel body, shared by the two entry kernels below.
 template <class C>
-__global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(C::WPE, C::WPE)))
-void fa_fwd_kernel(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, int a_batch, int a_hkv, int a_group, int a_nqt,
-                   int a_full, uint32_t a_mg, uint32_t a_mh, uint32_t a_mb, uint32_t a_shifts, FwdParams p) {
-  // The values the prologue needs first arrive as separate scalar arguments, which the command
-  // processor preloads into SGPRs before the first instruction (kernel-argument preloading, enabled at
-  // build time for the first 14 SGPRs of arguments); the rest of p is read from the argument block
-  // while the first loads are in flight.
-  p.q = a_q;
-  p.sq = a_sq;
-  p.sk = a_sk;
-  p.hq = a_hq;
-  p.batch = a_batch;
-  p.hkv = a_hkv;
-  p.group = a_group;
-  p.n_qtiles = a_nqt;
-  const WorkMap wm{a_group, a_hkv, a_batch, a_nqt, a_full, a_mg, a_mh, a_mb, a_shifts};
+__device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   using A = Attn<C>;
   constexpr int DQK = C::DQK, DV = C::DV, BN = C::BN, QB = C::QB;
 
@@ -511,7 +505,8 @@ void fa_fwd_kernel(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, int a_batc
   // Split mode: workgroup t takes part t / n_wg of work item t % n_wg.
   const int split = C::SPLIT ? (int)(blockIdx.x / p.n_wg) : 0;
   int b, g, member, qtile;
-  decode_workgroup(C::SPLIT ? blockIdx.x % (uint32_t)p.n_wg : blockIdx.x, wm, C::CAUSAL, b, g, member, qtile);
+  decode_workgroup<(C::OCC > 1)>(C::SPLIT ? blockIdx.x % (uint32_t)p.n_wg : blockIdx.x, wm, C::CAUSAL, b, g, member,
+                                 qtile);
   const int hq = g * p.group + member;
   const uint16_t* __restrict__ qh = p.q + (size_t)(b * p.hq + hq) * p.sq * DQK;
 
@@ -766,6 +761,35 @@ void fa_fwd_kernel(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, int a_batc
   }
 }
 
+// Entry kernels. The long instance reads everything from the argument block. The short instance,
+// whose workgroups are short chains on which the first loads' latency is felt, takes the values its
+// prologue needs first as leading scalar arguments, which the command processor preloads into SGPRs
+// before the first instruction (kernel-argument preloading, enabled at build time for the first 14
+// SGPRs of a kernel's leading scalar arguments), and issues its Q loads before it reads the argument
+// block. Preloading is kept off the long instance: it slows the launch of each wave, and on the 128K
+// workload the spread-out starts of the workgroups that stream one K/V head through an XCD's L2
+// doubled the L2 misses, at no gain in time.
+template <class C>
+__global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(C::WPE, C::WPE)))
+void fa_fwd_kernel(FwdParams p) {
+  fa_fwd_body<C>(p, WorkMap{p.group, p.hkv, p.batch, p.n_qtiles, p.full, p.m_group, p.m_hkv, p.m_batch, p.shifts});
+}
+template <class C>
+__global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(C::WPE, C::WPE)))
+void fa_fwd_kernel_preload(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, int a_batch, int a_hkv, int a_group,
+                           int a_nqt, int a_full, uint32_t a_mg, uint32_t a_mh, uint32_t a_mb, uint32_t a_shifts,
+                           FwdParams p) {
+  p.q = a_q;
+  p.sq = a_sq;
+  p.sk = a_sk;
+  p.hq = a_hq;
+  p.batch = a_batch;
+  p.hkv = a_hkv;
+  p.group = a_group;
+  p.n_qtiles = a_nqt;
+  fa_fwd_body<C>(p, WorkMap{a_group, a_hkv, a_batch, a_nqt, a_full, a_mg, a_mh, a_mb, a_shifts});
+}
+
 // The two instances. Long: 4 waves x 64 query rows (256 rows per workgroup), one workgroup per CU,
 // one wave per SIMD; the register budget of a wave (O 128 + Q 64 AGPRs at d = 128, two score tiles
 // and P in VGPRs) is what fixes 64 query rows per wave. K tiles are loaded two ahead: a third K slot
@@ -827,13 +851,22 @@ hipError_t launch_cfg(FwdParams p, hipStream_t stream) {
   p.n_qtiles = (p.sq + C::BM - 1) / C::BM;
   p.n_wg = p.batch * p.hq * p.n_qtiles;
   const int span = kNumXcd * p.group;
-  int full = (p.n_wg / span) * span;
-  FastDiv fg = make_fastdiv(p.group), fh = make_fastdiv(p.hkv), fb = make_fastdiv(p.batch);
-  uint32_t shifts = fg.sh | fh.sh << 6 | fb.sh << 12;
-  void* args[] = {&p.q,  &p.sq, &p.sk, &p.hq, &p.batch, &p.hkv, &p.group, &p.n_qtiles,
-                  &full, &fg.m, &fh.m, &fb.m, &shifts,  &p};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel<C>), dim3(p.n_wg * (C::SPLIT ? p.n_split : 1)),
-                         dim3(C::NT), args, 0, stream);
+  p.full = (p.n_wg / span) * span;
+  const FastDiv fg = make_fastdiv(p.group), fh = make_fastdiv(p.hkv), fb = make_fastdiv(p.batch);
+  p.m_group = fg.m;
+  p.m_hkv = fh.m;
+  p.m_batch = fb.m;
+  p.shifts = fg.sh | fh.sh << 6 | fb.sh << 12;
+  const dim3 grid(p.n_wg * (C::SPLIT ? p.n_split : 1));
+  if constexpr (C::OCC > 1) {
+    void* args[] = {&p.q,        &p.sq,   &p.sk,      &p.hq,    &p.batch,   &p.hkv,    &p.group,
+                    &p.n_qtiles, &p.full, &p.m_group, &p.m_hkv, &p.m_batch, &p.shifts, &p};
+    return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel_preload<C>), grid, dim3(C::NT), args, 0,
+                           stream);
+  } else {
+    void* args[] = {&p};
+    return hipLaunchKernel(reinterpret_cast<const void*>(&fa_fwd_kernel<C>), grid, dim3(C::NT), args, 0, stream);
+  }
 }
 
 template <int DQK, int DV, bool CAUSAL, bool SPLIT>

@@ -21,6 +21,10 @@ struct FwdParams {
                       // score stays infinite; negative when scale < 0
   int n_qtiles;       // ceil(Sq / block rows)
   int n_wg;           // work items (query blocks): batch * hq * n_qtiles
+  // Work decomposition constants (host-computed): the items in whole spans of 8 groups, and the
+  // multiply-high constants for dividing by group, hkv and batch, their shifts packed 6 bits apart.
+  int full;
+  uint32_t m_group, m_hkv, m_batch, shifts;
   // Split mode only: number of key-range parts, and the partial results, in the caller's workspace:
   // o_part fp32 [n_split][B][Hq][Sq][d_v] (O of each part normalised by its own row sum), lse_part
   // fp32 [n_split][B][Hq][Sq].
