@@ -195,21 +195,35 @@ struct WorkMap {
 template <bool FAST>
 __device__ __forceinline__ void decode_workgroup(uint32_t t, const WorkMap& w, bool causal, int& b, int& kvh,
                                                  int& member, int& qtile) {
-  const uint32_t G = w.group, H = w.hkv, Bt = w.batch;
-  auto div = [&](uint32_t n, uint32_t d, uint32_t m, uint32_t s) { return FAST ? fast_div(n, m, s) : n / d; };
-  const uint32_t sg = w.shifts & 63u, sh = (w.shifts >> 6) & 63u, sb = (w.shifts >> 12) & 63u;
-  uint32_t L = t;
-  if (t < (uint32_t)w.full) {
-    const uint32_t xcd = t % kNumXcd, slot = t / kNumXcd, sq = div(slot, G, w.m_group, sg);
-    L = (sq * kNumXcd + xcd) * G + (slot - sq * G);
+  if constexpr (FAST) {
+    const uint32_t G = w.group, sg = w.shifts & 63u, sh = (w.shifts >> 6) & 63u, sb = (w.shifts >> 12) & 63u;
+    uint32_t L = t;
+    if (t < (uint32_t)w.full) {
+      const uint32_t xcd = t % kNumXcd, slot = t / kNumXcd, sq = fast_div(slot, w.m_group, sg);
+      L = (sq * kNumXcd + xcd) * G + (slot - sq * G);
+    }
+    const uint32_t r = fast_div(L, w.m_group, sg);
+    member = (int)(L - r * G);
+    const uint32_t r2 = fast_div(r, w.m_hkv, sh);
+    kvh = (int)(r - r2 * (uint32_t)w.hkv);
+    const uint32_t qt = fast_div(r2, w.m_batch, sb);
+    b = (int)(r2 - qt * (uint32_t)w.batch);
+    qtile = causal ? w.n_qtiles - 1 - (int)qt : (int)qt;
+  } else {
+    const int G = w.group;
+    int L = (int)t;
+    if (L < w.full) {
+      const int xcd = L % kNumXcd, slot = L / kNumXcd;
+      L = ((slot / G) * kNumXcd + xcd) * G + slot % G;
+    }
+    member = L % G;
+    int r = L / G;
+    kvh = r % w.hkv;
+    r /= w.hkv;
+    b = r % w.batch;
+    const int qt = r / w.batch;
+    qtile = causal ? w.n_qtiles - 1 - qt : qt;
   }
-  const uint32_t r = div(L, G, w.m_group, sg);
-  member = (int)(L - r * G);
-  const uint32_t r2 = div(r, H, w.m_hkv, sh);
-  kvh = (int)(r - r2 * H);
-  const uint32_t qt = div(r2, Bt, w.m_batch, sb);
-  b = (int)(r2 - qt * Bt);
-  qtile = causal ? w.n_qtiles - 1 - (int)qt : (int)qt;
 }
 
 // Per-wave state and the math of the pipelined step.
