@@ -71,9 +71,7 @@ fa_status_t forward(const void* Q, const void* K, const void* V, void* O, float*
   const fa_status_t st = check_fused(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, d_qk, d_v, scale, causal, &cs);
   if (st != FA_OK) return st;
   if (B == 0 || Hq == 0 || Sq == 0) return FA_OK;
-  const int bm = fa::block_rows(d_qk, d_v, causal != 0);
-  const int64_t n_qtiles = (static_cast<int64_t>(Sq) + bm - 1) / bm;
-  const int64_t n_wg = static_cast<int64_t>(B) * Hq * n_qtiles;
+  const int64_t n_wg = fa::forward_workgroups(B, Hq, Hkv, Sq);
   if (n_wg > INT_MAX || static_cast<int64_t>(B) * Hq > INT_MAX || static_cast<int64_t>(B) * Hkv > INT_MAX)
     return FA_ERR_BAD_SHAPE;
   if (n_split > 0) {

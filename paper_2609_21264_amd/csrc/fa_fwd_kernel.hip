@@ -175,19 +175,22 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t m, uint32_t sh
   return (t + ((n - t) >> (sh & 1u))) >> (sh >> 1);
 }
 
-// What the work decomposition needs, all uniform over the launch: group size, key/value heads,
-// batch, query blocks per head, the items in whole XCD spans (below), and the fast divisions by the
-// group size, the key/value heads and the batch (their shifts packed 6 bits apart).
+// What the work decomposition needs, all uniform over the launch: workgroups per query block of one
+// key/value head (`group`: the GQA group size over the query heads a workgroup packs), key/value heads,
+// batch, query blocks per head, the items in whole XCD spans (below), and the fast divisions by
+// `group`, the key/value heads and the batch (their shifts packed 6 bits apart in bits 0-17; bits
+// 18-19 hold log2 of the query heads packed per workgroup).
 struct WorkMap {
   int group, hkv, batch, n_qtiles, full;
   uint32_t m_group, m_hkv, m_batch, shifts;
 };
 
-// Map a hardware workgroup index to (batch, key/value head, group member, query block). Workgroup t
-// runs on XCD t % 8. Logical work items are ordered heaviest query block first (causal), then batch,
-// key/value head and group member; each group of `group` consecutive items (the query heads of one
-// key/value head at one query block) is placed on one XCD, and groups go to XCDs round-robin
-// (`full` = the items in whole spans of 8 groups; the rest keep their order). FAST divides through
+// Map a hardware workgroup index to (batch, key/value head, member, query block); the member selects
+// which of the key/value head's query heads the workgroup takes. Workgroup t runs on XCD t % 8.
+// Logical work items are ordered heaviest query block first (causal), then batch, key/value head and
+// member; each group of `group` consecutive items (the workgroups of one key/value head at one query
+// block) is placed on one XCD, and groups go to XCDs round-robin (`full` = the items in whole spans of
+// 8 groups; the rest keep their order). FAST divides through
 // the multiply-high constants, else with the compiler's division sequence (the long instance: there
 // the faster prologue measured no gain in time, and on the 128K workload it shifted the relative
 // start times of the workgroups that stream one K/V head through an XCD's L2 enough to double the L2
@@ -521,18 +524,26 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   int b, g, member, qtile;
   decode_workgroup<(C::OCC > 1)>(C::SPLIT ? blockIdx.x % (uint32_t)p.n_wg : blockIdx.x, wm, C::CAUSAL, b, g, member,
                                  qtile);
-  const int hq = g * p.group + member;
+  // Query heads packed per workgroup (HW = 1, 2 or 4, the largest that divides the GQA group size):
+  // the waves split into HW heads of the same key/value head, each taking NWAVES / HW consecutive
+  // 32*QB-row chunks of the block's rows, so that all heads of the workgroup share every K/V tile
+  // and, when HW = NWAVES, every wave visits the same key tiles (no wave idles through the tiles of
+  // a causal diagonal that its rows do not see).
+  const int hw_log = (int)((wm.shifts >> 18) & 3u);
+  const int rw = C::NWAVES >> hw_log;                    // row chunks per head
+  const int bmr = rw * 32 * QB;                          // query rows of the block
+  const int hq = g * p.group + (member << hw_log) + wave / rw;
   const uint16_t* __restrict__ qh = p.q + (size_t)(b * p.hq + hq) * p.sq * DQK;
 
-  const int q0 = qtile * C::BM;
-  st.qw = q0 + wave * 32 * QB;  // first query row of this wave
+  const int q0 = qtile * bmr;
+  st.qw = q0 + (wave % rw) * 32 * QB;  // first query row of this wave
   st.diag = p.sk - p.sq;        // key j is visible to query i iff j <= i + diag
 
   // Key tiles this workgroup visits, and how many leading ones need no mask for any of its rows.
   int kv_end = p.sk;
   int n_plain = p.sk / BN;
   if (C::CAUSAL) {
-    const int last_row = min(q0 + C::BM, p.sq) - 1;
+    const int last_row = min(q0 + bmr, p.sq) - 1;
     kv_end = max(0, min(p.sk, last_row + st.diag + 1));
     n_plain = min(n_plain, max(0, q0 + st.diag + 1) / BN);
   }
@@ -786,7 +797,8 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
 template <class C>
 __global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(C::WPE, C::WPE)))
 void fa_fwd_kernel(FwdParams p) {
-  fa_fwd_body<C>(p, WorkMap{p.group, p.hkv, p.batch, p.n_qtiles, p.full, p.m_group, p.m_hkv, p.m_batch, p.shifts});
+  fa_fwd_body<C>(p, WorkMap{p.group >> ((p.shifts >> 18) & 3u), p.hkv, p.batch, p.n_qtiles, p.full, p.m_group, p.m_hkv,
+                            p.m_batch, p.shifts});
 }
 template <class C>
 __global__ __attribute__((amdgpu_flat_work_group_size(C::NT, C::NT), amdgpu_waves_per_eu(C::WPE, C::WPE)))
@@ -801,7 +813,8 @@ void fa_fwd_kernel_preload(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, in
   p.hkv = a_hkv;
   p.group = a_group;
   p.n_qtiles = a_nqt;
-  fa_fwd_body<C>(p, WorkMap{a_group, a_hkv, a_batch, a_nqt, a_full, a_mg, a_mh, a_mb, a_shifts});
+  fa_fwd_body<C>(p, WorkMap{a_group >> ((a_shifts >> 18) & 3u), a_hkv, a_batch, a_nqt, a_full, a_mg, a_mh, a_mb,
+                            a_shifts});
 }
 
 // The two instances. Long: 4 waves x 64 query rows (256 rows per workgroup), one workgroup per CU,
@@ -860,17 +873,28 @@ bool use_short(const FwdParams& p, int d_qk, int d_v) {
   return blocks <= kShortMaxBlocks;
 }
 
+// log2 of the query heads a workgroup of `nwaves` waves packs: 4, 2 or 1 heads, the largest that
+// divides the GQA group size (and the wave count).
+int packed_heads_log2(int group, int nwaves) {
+  if (group % 4 == 0 && nwaves % 4 == 0) return 2;
+  if (group % 2 == 0 && nwaves % 2 == 0) return 1;
+  return 0;
+}
+
 template <class C>
 hipError_t launch_cfg(FwdParams p, hipStream_t stream) {
-  p.n_qtiles = (p.sq + C::BM - 1) / C::BM;
-  p.n_wg = p.batch * p.hq * p.n_qtiles;
-  const int span = kNumXcd * p.group;
+  const int hw_log = packed_heads_log2(p.group, C::NWAVES);
+  const int gi = p.group >> hw_log;  // workgroups per key/value head and query block
+  const int bmr = (C::NWAVES >> hw_log) * 32 * C::QB;
+  p.n_qtiles = (p.sq + bmr - 1) / bmr;
+  p.n_wg = p.batch * p.hkv * gi * p.n_qtiles;
+  const int span = kNumXcd * gi;
   p.full = (p.n_wg / span) * span;
-  const FastDiv fg = make_fastdiv(p.group), fh = make_fastdiv(p.hkv), fb = make_fastdiv(p.batch);
+  const FastDiv fg = make_fastdiv(gi), fh = make_fastdiv(p.hkv), fb = make_fastdiv(p.batch);
   p.m_group = fg.m;
   p.m_hkv = fh.m;
   p.m_batch = fb.m;
-  p.shifts = fg.sh | fh.sh << 6 | fb.sh << 12;
+  p.shifts = fg.sh | fh.sh << 6 | fb.sh << 12 | (uint32_t)hw_log << 18;
   const dim3 grid(p.n_wg * (C::SPLIT ? p.n_split : 1));
   if constexpr (C::OCC > 1) {
     void* args[] = {&p.q,        &p.sq,   &p.sk,      &p.hq,    &p.batch,   &p.hkv,    &p.group,
@@ -968,6 +992,14 @@ int block_rows(int d_qk, int d_v, bool causal) {
   if (d_qk == 128 && d_v == 128) return Instance<128, 128, false>::C::BM;
   if (d_qk == 192 && d_v == 128) return Instance<192, 128, false>::C::BM;
   return 0;
+}
+
+int64_t forward_workgroups(int batch, int hq, int hkv, int sq) {
+  // the long instance's grid (the short instance runs only grids of at most 512 workgroups)
+  using C = Instance<64, 64, false>::C;
+  const int group = hq / hkv, hw_log = packed_heads_log2(group, C::NWAVES);
+  const int64_t bmr = (C::NWAVES >> hw_log) * 32 * C::QB;
+  return (int64_t)batch * hkv * (group >> hw_log) * ((sq + bmr - 1) / bmr);
 }
 
 hipError_t launch_forward(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream) {

@@ -43,10 +43,14 @@ struct MergeParams {
   int n_split;
 };
 
-// Query rows per workgroup of the long kernel instance for (d_qk, d_v, causal) (split mode, and
-// problems with more than 256 such blocks); 0 if not compiled in. Problems with fewer blocks at
-// d = 64 or 128 run the short instance, with half as many rows per workgroup.
+// Query rows per workgroup of the long kernel instance for (d_qk, d_v, causal) when a workgroup holds
+// one query head (split mode, and problems with more than 256 such blocks); 0 if not compiled in.
+// With a GQA group size divisible by 2 or 4 a workgroup holds as many query heads, each with half or
+// a quarter of these rows. Problems with at most 256 blocks at d = 64 or 128 run the short instance,
+// with half as many rows per workgroup.
 int block_rows(int d_qk, int d_v, bool causal);
+// Workgroups of the long instance's grid (one part per query block and packed heads).
+int64_t forward_workgroups(int batch, int hq, int hkv, int sq);
 
 // Enqueue the forward kernel for (d_qk, d_v, causal) on `stream`. Requires Sq > 0, B*Hq > 0 and a
 // grid that fits; fills n_qtiles / n_wg itself. Returns the launch status of the HIP runtime.
