@@ -1,11 +1,14 @@
-// Fused attention forward for gfx950 (MI355X): one kernel computes, per (batch, query head, block of
+// Fused attention forward for gfx950 (MI355X): one kernel computes, per (batch, query heads, block of
 // query rows), O = softmax(scale * Q K^T) V with the online softmax of the paper's per-tile algorithm
 // (Alg. 1, Sec. 2.1): key/value rows are streamed in tiles, each query row keeps a reference maximum
 // and a running sum, and the unnormalised output accumulator is rescaled when the reference moves.
 // Scores and probabilities live only in registers; K and V tiles are staged in LDS.
 //
 // Mapping onto CDNA4:
-//  * A workgroup has NWAVES = 4 wavefronts (one per SIMD); each wave owns 32*QB = 64 query rows.
+//  * A workgroup has NWAVES = 4 wavefronts (one per SIMD) sharing one key/value head; each wave owns
+//    32*QB = 64 query rows of one query head: 256 rows of one head, or 128 rows of 2 heads or 64 rows
+//    of 4 heads of the same GQA group when the group size allows (long instance; the short instance
+//    has 32-row waves and two workgroups per CU).
 //  * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the K tile (LDS)
 //    is the A operand and the wave's Q rows (AGPRs, loaded once) are the B operand. In the 32x32
 //    accumulator a lane then holds ONE query row (column = lane % 32) and 16 keys, so row
@@ -33,9 +36,9 @@
 //    probabilities and LDS fragments use VGPRs.
 //  * Causal masking skips key tiles above the diagonal entirely and applies the element mask only on
 //    diagonal and tail tiles.
-//  * Workgroup order: heaviest query blocks first when causal, and the Hq/Hkv query heads that share
-//    a key/value head are dispatched consecutively onto the same XCD (workgroup IDs are assigned to
-//    the 8 XCDs round-robin), so their K/V tiles are served from one L2.
+//  * Workgroup order: heaviest query blocks first when causal, and the workgroups that share a
+//    key/value head at one query block are dispatched consecutively onto the same XCD (workgroup IDs
+//    are assigned to the 8 XCDs round-robin), so their K/V tiles are served from one L2.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
