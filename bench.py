@@ -53,11 +53,38 @@ KERNEL_SOURCES = ["paper_2609_21264_amd/csrc/fa_fwd_kernel.hip", "paper_2609_212
                   "paper_2609_21264_amd/csrc/fa_device.h"]
 
 
+def _code_tokens(text: str) -> str:
+    """The source with its comments removed and every run of whitespace made one space: what the
+    compiler sees, so that editing a comment does not orphan the profiles measured on that code."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":  # string or character literal, copied through its closing quote
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            out.append(" ")
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
+    """sha256[:16] of the device sources' code (comments and layout ignored)."""
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(_code_tokens(f.read()).encode())
+        h.update(b"\0")
     return h.hexdigest()[:16]
 
 

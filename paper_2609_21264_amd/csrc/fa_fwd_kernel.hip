@@ -135,7 +135,7 @@ struct Cfg {
   // Waves per SIMD the registers are budgeted for: the workgroup's own (4 SIMDs per CU) times the
   // workgroups that share a CU (OCC_).
   static constexpr int WPE = (NWAVES > 4 ? NWAVES / 4 : 1) * OCC_;
-  static constexpr int BM = NWAVES * 32 * QB;  // query rows per workgroup
+  static constexpr int BM = NWAVES * 32 * QB;  // query rows per workgroup holding one query head
   static constexpr int KCH = DQK / 8;          // 16-byte chunks per K-tile row
   static constexpr int VCH = DV / 8;           // 16-byte chunks per V-tile row
   static constexpr int K_BYTES = BN * DQK * 2;
@@ -820,11 +820,11 @@ void fa_fwd_kernel_preload(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, in
                             a_shifts});
 }
 
-// The two instances. Long: 4 waves x 64 query rows (256 rows per workgroup), one workgroup per CU,
+// The two instances. Long: 4 waves x 64 query rows (256 row-heads per workgroup), one workgroup per CU,
 // one wave per SIMD; the register budget of a wave (O 128 + Q 64 AGPRs at d = 128, two score tiles
 // and P in VGPRs) is what fixes 64 query rows per wave. K tiles are loaded two ahead: a third K slot
 // measured 2-3 % slower on the 8K, 4K-d192 and 128K prefill shapes (one box, interleaved).
-// Short: 4 waves x 32 query rows (128 rows per workgroup), two workgroups per CU (two waves per SIMD,
+// Short: 4 waves x 32 query rows (128 row-heads per workgroup), two workgroups per CU (two waves per SIMD,
 // 256 registers each, O and Q in VGPRs), shallower fragment prefetch at d = 128 so that the step fits
 // the registers without spilling, and a V ring of 3 slots at d = 128 (so that two rings fit one CU's
 // LDS) and 4 at d = 64 (V tiles loaded two steps ahead; 3-8 % faster than 3 slots on the d = 64

@@ -55,3 +55,13 @@ def test_cpu_baseline_whole_heads_and_row_subset():
     rows = W.sample_rows(long, n=64)[0]
     assert res["rows_timed"] == len(rows) and "seeded subsets" in res["sample"]
     assert abs(res["extrapolated_s"] - res["measured_s"] * 12000 / len(rows)) <= 0.1 + 1e-3 * res["extrapolated_s"]
+
+
+def test_code_hash_ignores_comments_and_layout_but_not_code():
+    code = 'int f(int x) {\n  return x + 1;  // one more\n}\n/* block\n comment */ const char* s = "a // b /* c */";\n'
+    same = '// header comment\nint f(int x)\n{\n    return x + 1;\n}\nconst char* s = "a // b /* c */";   /* x */\n'
+    assert bench._code_tokens(code) == bench._code_tokens(same)
+    # a change inside a string literal or to the code itself is seen
+    assert bench._code_tokens(code) != bench._code_tokens(code.replace("a // b", "a // c"))
+    assert bench._code_tokens(code) != bench._code_tokens(code.replace("x + 1", "x + 2"))
+    assert len(bench.kernel_source_hash()) == 16
