@@ -274,11 +274,12 @@ fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
 const char* fa_status_str(fa_status_t s);
 
 /* Query rows per workgroup of the fused kernel for the given head dimensions when a workgroup holds
- * one query head, as split mode and problems with more than 256 such blocks (B * Hq * ceil(Sq / rows))
- * run it; 0 if unsupported. When Hq / Hkv is divisible by 2 or 4 a workgroup holds that many query
- * heads of one key/value head with a half or a quarter of these rows each. Other problems at
- * (d_qk, d_v) = (64, 64) or (128, 128) run workgroups of half as many rows, two per compute unit, so
- * that few query blocks still occupy the GPU. Host arithmetic only. */
+ * one query head, as split mode and problems with more such blocks (B * Hq * ceil(Sq / rows)) than
+ * 1024 at (d_qk, d_v) = (64, 64) or 256 at (128, 128) run it, and every (192, 128) problem; 0 if
+ * unsupported. When Hq / Hkv is divisible by 2 or 4 a workgroup holds that many query heads of one
+ * key/value head with a half or a quarter of these rows each. The other problems at (64, 64) or
+ * (128, 128) run workgroups of half as many rows, two per compute unit, so that few query blocks
+ * still occupy the GPU. Host arithmetic only. */
 int fa_block_rows(int d_qk, int d_v, int causal);
 
 #ifdef __cplusplus

@@ -44,10 +44,11 @@ struct MergeParams {
 };
 
 // Query rows per workgroup of the long kernel instance for (d_qk, d_v, causal) when a workgroup holds
-// one query head (split mode, and problems with more than 256 such blocks); 0 if not compiled in.
+// one query head (split mode, and problems with more such blocks than the short instance takes); 0 if
+// not compiled in.
 // With a GQA group size divisible by 2 or 4 a workgroup holds as many query heads, each with half or
-// a quarter of these rows. Problems with at most 256 blocks at d = 64 or 128 run the short instance,
-// with half as many rows per workgroup.
+// a quarter of these rows. Problems with at most 1024 blocks at d = 64 or 256 at d = 128 run the
+// short instance, with half as many rows per workgroup.
 int block_rows(int d_qk, int d_v, bool causal);
 // Workgroups of the long instance's grid (one part per query block and packed heads).
 int64_t forward_workgroups(int batch, int hq, int hkv, int sq);

@@ -20,8 +20,9 @@ pytestmark = pytest.mark.gpu
 # name: (B, Hq, Hkv, Sq, Sk, d_qk, d_v, causal, call)
 CASES = {
     "fused": (1, 4, 2, 300, 300, 128, 128, True, lambda q, k, v, c: fa.forward(q, k, v, causal=c, return_lse=True)),
-    # more than 256 query blocks of 256 rows: the long instance (the case above runs the short one)
-    "fused-long": (1, 264, 66, 130, 200, 64, 64, False,
+    # more than 256 query blocks of 256 rows at d = 128: the long instance (the case above runs the
+    # short one)
+    "fused-long": (1, 264, 66, 130, 200, 128, 128, False,
                    lambda q, k, v, c: fa.forward(q, k, v, causal=c, return_lse=True)),
     "fused-d192": (2, 2, 1, 130, 200, 192, 128, False,
                    lambda q, k, v, c: fa.forward(q, k, v, causal=c, return_lse=True)),

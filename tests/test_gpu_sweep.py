@@ -5,7 +5,7 @@ The hand-picked edge cases of the other GPU test files cover what each code path
 on; this file draws many more combinations of the same parameters at once (head dimensions, GQA
 group size, batch, ragged query and key lengths, causal masking, scale and input spread) from a fixed
 seed, so that an interaction nobody thought of still meets the oracle. A quarter of the fused cases
-carry enough heads for more than 256 query blocks of 256 rows, so both kernel instances are drawn.
+carry enough heads for the long instance, so both kernel instances are drawn.
 """
 
 import numpy as np
@@ -20,6 +20,7 @@ from parity import compare, rounding_bar, to_f64
 pytestmark = pytest.mark.gpu
 
 DIMS = [(64, 64), (128, 128), (192, 128)]
+SHORT_MAX = {64: 1024, 128: 256}  # largest block count (256 rows) that runs the short instance
 GROUPS = [1, 2, 3, 4, 7, 8]
 
 
@@ -41,10 +42,10 @@ def _draw(rng, idx, kind):
     else:
         sq = _length(rng, 1, 700)
         sk = sq if rng.uniform() < 0.4 else _length(rng, 1, 700)
-        if rng.uniform() < 0.25:  # more than 256 blocks of 256 rows: the long instance
+        if rng.uniform() < 0.25:  # past the short instance's largest grid: the long instance
             sq = min(sq, 300)
             sk = min(sk, 300)
-            b, hkv = 1, -(-257 // (g * -(-sq // 256)))
+            b, hkv = 1, -(-(SHORT_MAX.get(dqk, 256) + 1) // (g * -(-sq // 256)))
     scale = None if rng.uniform() < 0.7 else float(rng.uniform(-0.3, 0.5))
     sigma = float(rng.choice([1.0, 1.0, 0.5, 2.0]))
     seed = 5000 + 100 * ["fused", "split", "decode"].index(kind) + idx
@@ -79,7 +80,9 @@ def _check(w, **kw):
 
 def test_sweep_draws_both_instances_and_every_head_dimension():
     blocks = [w.B * w.Hq * -(-w.Sq // fa.fa_block_rows(w.dqk, w.dv, w.causal)) for w in FUSED]
-    assert any(n > 256 for n in blocks) and any(n <= 256 for n in blocks)
+    short = [w.dqk in SHORT_MAX and n <= SHORT_MAX[w.dqk] for w, n in zip(FUSED, blocks)]
+    assert any(short) and not all(short)
+    assert any(not s and w.dqk == 64 for s, w in zip(short, FUSED))
     assert {(w.dqk, w.dv) for w in FUSED} == set(DIMS)
     assert len(DECODE) == 48 and all(w.Sq <= 20 for w in DECODE)
 
