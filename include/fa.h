@@ -273,14 +273,24 @@ fa_status_t fa_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
 /* Static, human-readable name of a status code ("FA_OK", ...); "unknown status" otherwise. */
 const char* fa_status_str(fa_status_t s);
 
-/* Query rows per workgroup of the fused kernel for the given head dimensions when a workgroup holds
- * one query head, as split mode and problems with more such blocks (B * Hq * ceil(Sq / rows)) than
- * 1024 at (d_qk, d_v) = (64, 64) or 256 at (128, 128) run it, and every (192, 128) problem; 0 if
- * unsupported. When Hq / Hkv is divisible by 2 or 4 a workgroup holds that many query heads of one
- * key/value head with a half or a quarter of these rows each. The other problems at (64, 64) or
- * (128, 128) run workgroups of half as many rows, two per compute unit, so that few query blocks
- * still occupy the GPU. Host arithmetic only. */
+/* Query rows per workgroup of the fused kernel's long instance for the given head dimensions when a
+ * workgroup holds one query head (256); 0 if unsupported. It runs split mode, every (192, 128)
+ * problem, and problems at (d_qk, d_v) = (64, 64) or (128, 128) with more such blocks
+ * (B * Hq * ceil(Sq / rows)) than the other instances take (fa_fwd_rows). When Hq / Hkv is divisible
+ * by 2 or 4 a workgroup holds that many query heads of one key/value head with a half or a quarter of
+ * these rows each. Host arithmetic only. */
 int fa_block_rows(int d_qk, int d_v, int causal);
+
+/* Query rows per workgroup holding one query head of the fused-kernel instance that fa_fwd and
+ * fa_fwd_ex (without split mode) launch for a problem of B batches, Hq query heads and Sq query rows:
+ * 256 (long instance: one workgroup per compute unit), 128 (short instance: two per compute unit, at
+ * most 1024 blocks at d = 64 and 256 at d = 128, i.e. blocks of the long instance's rows) or 64 (key
+ * halves: each half of a workgroup's waves takes one half of every key tile, and the halves are
+ * merged at the end; causal problems of at most 320 blocks at d = 64 and 256 at d = 128, others of at
+ * most 64 and 128). Every instance computes the same function (Eq. (1) by Alg. 1); which one runs
+ * follows from the grid size alone. 0 for unsupported head dimensions or negative sizes. Host
+ * arithmetic only. */
+int fa_fwd_rows(int B, int Hq, int Sq, int d_qk, int d_v, int causal);
 
 #ifdef __cplusplus
 }

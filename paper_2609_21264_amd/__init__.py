@@ -5,7 +5,7 @@ supplies device memory and the stream; every step of the computation runs in the
 kernel. The functions below marshal arguments and translate status codes, nothing more.
 
 * :func:`fa_fwd`, :func:`fa_fwd_ex`, :func:`fa_fwd_split`, :func:`fa_fwd_split_workspace_bytes`,
-  :func:`fa_status_str`, :func:`fa_block_rows` -- the C entry points under the same names, taking raw
+  :func:`fa_status_str`, :func:`fa_block_rows`, :func:`fa_fwd_rows` -- the C entry points under the same names, taking raw
   device pointers (ints) and sizes.
 * :func:`fa_lbl_scores`, :func:`fa_lbl_softmax`, :func:`fa_lbl_pv`, :func:`fa_lbl_ld`,
   :func:`fa_lbl_workspace_bytes`, :func:`fa_fwd_unfused` -- the layer-by-layer (unfused) operators
@@ -28,7 +28,7 @@ from ._lib import (FA_ERR_BAD_SCALE, FA_ERR_BAD_SHAPE, FA_ERR_HIP, FA_ERR_NULL_P
                    FA_ERR_UNSUPPORTED, FA_ERR_WORKSPACE, FA_NOALLOC_SCRATCH_BYTES, FA_OK, LIB_PATH)
 
 __all__ = ["fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
-           "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
+           "fa_status_str", "fa_block_rows", "fa_fwd_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
            "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts",
            "fa_fwd_decode_noalloc", "forward", "forward_unfused", "FaError", "LIB_PATH", "FA_NOALLOC_SCRATCH_BYTES"]
 
@@ -47,6 +47,10 @@ def fa_status_str(status: int) -> str:
 
 def fa_block_rows(d_qk: int, d_v: int, causal: bool) -> int:
     return int(_lib.load().fa_block_rows(int(d_qk), int(d_v), int(bool(causal))))
+
+
+def fa_fwd_rows(B: int, Hq: int, Sq: int, d_qk: int, d_v: int, causal: bool) -> int:
+    return int(_lib.load().fa_fwd_rows(int(B), int(Hq), int(Sq), int(d_qk), int(d_v), int(bool(causal))))
 
 
 def fa_fwd(Q: int, K: int, V: int, O: int, B: int, Hq: int, Hkv: int, Sq: int, Sk: int, d: int,

@@ -26,7 +26,7 @@ FA_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 #: Symbols include/fa.h declares.
 EXPORTED = ("fa_fwd", "fa_fwd_ex", "fa_fwd_split", "fa_fwd_split_workspace_bytes", "fa_fwd_split_parts",
-            "fa_status_str", "fa_block_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
+            "fa_status_str", "fa_block_rows", "fa_fwd_rows", "fa_lbl_scores", "fa_lbl_softmax", "fa_lbl_pv", "fa_lbl_ld",
             "fa_lbl_workspace_bytes", "fa_fwd_unfused", "fa_fwd_decode", "fa_fwd_decode_parts",
             "fa_fwd_decode_noalloc")
 
@@ -59,6 +59,8 @@ def load() -> ctypes.CDLL:
     lib.fa_status_str.restype = ctypes.c_char_p
     lib.fa_block_rows.argtypes = [i, i, i]
     lib.fa_block_rows.restype = i
+    lib.fa_fwd_rows.argtypes = [i, i, i, i, i, i]
+    lib.fa_fwd_rows.restype = i
     lib.fa_lbl_scores.argtypes = [vp, vp, vp, i, i, i, i, i, i, f, i, vp]
     lib.fa_lbl_scores.restype = i
     lib.fa_lbl_softmax.argtypes = [vp, vp, vp, i, i, i, i, i, vp]

@@ -454,4 +454,8 @@ const char* fa_status_str(fa_status_t s) {
 
 int fa_block_rows(int d_qk, int d_v, int causal) { return fa::block_rows(d_qk, d_v, causal != 0); }
 
+int fa_fwd_rows(int B, int Hq, int Sq, int d_qk, int d_v, int causal) {
+  return fa::instance_rows(B, Hq, Sq, d_qk, d_v, causal != 0);
+}
+
 }  // extern "C"

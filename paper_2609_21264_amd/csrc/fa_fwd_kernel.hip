@@ -8,7 +8,8 @@
 //  * A workgroup has NWAVES = 4 wavefronts (one per SIMD) sharing one key/value head; each wave owns
 //    32*QB = 64 query rows of one query head: 256 rows of one head, or 128 rows of 2 heads or 64 rows
 //    of 4 heads of the same GQA group when the group size allows (long instance; the short instance
-//    has 32-row waves and two workgroups per CU).
+//    has 32-row waves and two workgroups per CU, and the key-halves instance two sets of two 32-row
+//    waves that split every key tile between them, with two or three workgroups per CU).
 //  * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the K tile (LDS)
 //    is the A operand and the wave's Q rows (AGPRs, loaded once) are the B operand. In the 32x32
 //    accumulator a lane then holds ONE query row (column = lane % 32) and 16 keys, so row
@@ -120,11 +121,16 @@ __device__ __forceinline__ void q_ready(bf16x8& r) {
 
 // Compile-time configuration of one kernel instance: head dimensions, key-tile width, waves per
 // workgroup, 32-row query blocks per wave, causal masking, split mode, workgroups sharing a CU (OCC),
-// K and V fragments read ahead from LDS (KPF, VPF), and K and V ring slots in LDS (NKR, NVR).
+// K and V fragments read ahead from LDS (KPF, VPF), K and V ring slots in LDS (NKR, NVR), and the
+// parts each key tile is split into between the waves (KSPLIT).
 template <int DQK_, int DV_, int BN_, int NWAVES_, int QB_, bool CAUSAL_, bool SPLIT_, int OCC_, int KPF_, int VPF_,
-          int NKR_, int NVR_>
+          int NKR_, int NVR_, int KSPLIT_ = 1>
 struct Cfg {
   static constexpr int DQK = DQK_, DV = DV_, BN = BN_, NWAVES = NWAVES_, QB = QB_;
+  // KSPLIT = 2: the waves form two sets of NWAVES / 2 (RWAVES) that own the same query rows; set k
+  // takes the k-th 32-key half of every key tile (WBN keys per wave and tile), and the two partial
+  // results of each row are merged in LDS at the end.
+  static constexpr int KSPLIT = KSPLIT_, RWAVES = NWAVES / KSPLIT_, WBN = BN_ / KSPLIT_;
   static constexpr int KPF = KPF_, VPF = VPF_;
   static constexpr int OCC = OCC_;  // workgroups sharing a CU
   static constexpr bool CAUSAL = CAUSAL_;
@@ -135,7 +141,7 @@ struct Cfg {
   // Waves per SIMD the registers are budgeted for: the workgroup's own (4 SIMDs per CU) times the
   // workgroups that share a CU (OCC_).
   static constexpr int WPE = (NWAVES > 4 ? NWAVES / 4 : 1) * OCC_;
-  static constexpr int BM = NWAVES * 32 * QB;  // query rows per workgroup holding one query head
+  static constexpr int BM = RWAVES * 32 * QB;  // query rows per workgroup holding one query head
   static constexpr int KCH = DQK / 8;          // 16-byte chunks per K-tile row
   static constexpr int VCH = DV / 8;           // 16-byte chunks per V-tile row
   static constexpr int K_BYTES = BN * DQK * 2;
@@ -156,6 +162,7 @@ struct Cfg {
   static_assert(NKR >= 2 && NKR + 1 <= NVR && NVR <= NKR + 2, "ring sizes");
   static_assert(KA * (K_LOADS + V_LOADS) < 64 && VA * (K_LOADS + V_LOADS) < 64, "vmcnt range");
   static_assert(LDS_BYTES * OCC_ <= 163840, "LDS budget of the workgroups sharing a CU");
+  static_assert(KSPLIT == 1 || (KSPLIT == 2 && !SPLIT && NWAVES % 2 == 0), "key halves: two wave sets, not split mode");
 };
 
 // Division by a divisor that is fixed for the launch, as a multiply-high and two shifts (Granlund and
@@ -243,7 +250,7 @@ __device__ __forceinline__ void decode_workgroup(uint32_t t, const WorkMap& w, b
 // score that has been seen.
 template <class C>
 struct Attn {
-  static constexpr int DQK = C::DQK, DV = C::DV, BN = C::BN, QB = C::QB;
+  static constexpr int DQK = C::DQK, DV = C::DV, BN = C::WBN, QB = C::QB;  // BN: this wave's keys of a tile
   static constexpr int KS = DQK / 16;  // k-steps of the score product
   static constexpr int KB = BN / 32;   // 32-key blocks per tile
   static constexpr int DB = DV / 32;   // 32-dim blocks of the output
@@ -532,14 +539,18 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   // 32*QB-row chunks of the block's rows, so that all heads of the workgroup share every K/V tile
   // and, when HW = NWAVES, every wave visits the same key tiles (no wave idles through the tiles of
   // a causal diagonal that its rows do not see).
+  // With key halves (KSPLIT = 2) the same applies within each wave set: wave w belongs to set
+  // w / RWAVES, which takes keys [kpart, kpart + WBN) of every tile, and to row chunk w % RWAVES.
   const int hw_log = (int)((wm.shifts >> 18) & 3u);
-  const int rw = C::NWAVES >> hw_log;                    // row chunks per head
+  const int kset = wave / C::RWAVES, rwave = wave % C::RWAVES;
+  const int kpart = kset * C::WBN;                       // first key of this wave's part of a tile
+  const int rw = C::RWAVES >> hw_log;                    // row chunks per head
   const int bmr = rw * 32 * QB;                          // query rows of the block
-  const int hq = g * p.group + (member << hw_log) + wave / rw;
+  const int hq = g * p.group + (member << hw_log) + rwave / rw;
   const uint16_t* __restrict__ qh = p.q + (size_t)(b * p.hq + hq) * p.sq * DQK;
 
   const int q0 = qtile * bmr;
-  st.qw = q0 + (wave % rw) * 32 * QB;  // first query row of this wave
+  st.qw = q0 + (rwave % rw) * 32 * QB;  // first query row of this wave
   st.diag = p.sk - p.sq;        // key j is visible to query i iff j <= i + diag
 
   // Key tiles this workgroup visits, and how many leading ones need no mask for any of its rows.
@@ -588,6 +599,10 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   vload.init(vh, kv_lim, wave, lane, vswz);
   auto kslot = [&](int t) { return smem + (t % C::NKR) * C::K_BYTES; };
   auto vslot = [&](int t) { return smem + C::NKR * C::K_BYTES + (t % C::NVR) * C::V_BYTES; };
+  // This wave's keys of tile t (rows kpart .. kpart + WBN - 1 of the slot). The K and V swizzles
+  // repeat every 32 rows, so a part starting at row 32 reads like a tile of its own.
+  auto kmine = [&](int t) { return kslot(t) + kpart * (DQK * 2); };
+  auto vmine = [&](int t) { return vslot(t) + kpart * (DV * 2); };
 #pragma unroll
   for (int g = -C::KA; g < 0; ++g) {
     kload.issue(kb0 + (g + C::KA) * BN, kslot(g + C::KA), wave);
@@ -621,8 +636,8 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    st.scores(sA, kslot(0));
-    if (n_plain == 0) st.mask_tile(sA, kb0);
+    st.scores(sA, kmine(0));
+    if (n_plain == 0) st.mask_tile(sA, kb0 + kpart);
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) st.m_run[qb] = st.row_max(sA, qb);
 #pragma unroll
@@ -659,15 +674,15 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   int j = 0;
   for (; j + 1 < nt; j += 2) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, kb0 + j * BN,
-            issue);
+    st.step(sA, sB, pA, pB, kmine(j + 1), j > 0 ? vmine(j - 1) : kmine(1), j > 0 && j >= n_plain,
+            kb0 + j * BN + kpart, issue);
     sync_step(j + 1);
-    st.step(sB, sA, pB, pA, kslot(j + 2), vslot(j), j + 1 >= n_plain, kb0 + (j + 1) * BN, issue);
+    st.step(sB, sA, pB, pA, kmine(j + 2), vmine(j), j + 1 >= n_plain, kb0 + (j + 1) * BN + kpart, issue);
   }
   if (j < nt) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kslot(j + 1), j > 0 ? vslot(j - 1) : kslot(1), j > 0 && j >= n_plain, kb0 + j * BN,
-            issue);
+    st.step(sA, sB, pA, pB, kmine(j + 1), j > 0 ? vmine(j - 1) : kmine(1), j > 0 && j >= n_plain,
+            kb0 + j * BN + kpart, issue);
   }
   if (nt > 0) {
     // P V of the last tile, on a selected copy of P: two calls would leave O in different
@@ -687,7 +702,7 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int r = 0; r < 8; ++r) pl[kb][qb][r] = (pA[kb][qb][r] & take_a) | (pB[kb][qb][r] & ~take_a);
-    st.pv_tile(pl, vslot(nt - 1));
+    st.pv_tile(pl, vmine(nt - 1));
   }
 
   // No load may still be writing this workgroup's LDS when it exits (the prologue issues loads even
@@ -697,6 +712,59 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   compiler_fence();
   __builtin_amdgcn_s_barrier();
   compiler_fence();
+
+  if constexpr (C::KSPLIT > 1) {
+    // Merge of the two key halves (the combination step of Alg. 2 inside the workgroup): the second
+    // wave set hands its O, reference maxima and lane row sums to the wave of the first set with the
+    // same rows through LDS, lane by lane (both hold the same rows and dims in the same registers),
+    // and exits. With m = max(m_a, m_b): O = O_a 2^(m_a - m) + O_b 2^(m_b - m), likewise l; a half
+    // that saw no visible key (m = -inf, O = 0, l = 0) gets weight 0. The exchange area lies past
+    // the first set's output staging tiles.
+    constexpr int NF = A::DB * QB * 16;  // O floats per lane
+    constexpr int XCH_OFF = C::RWAVES * 32 * QB * DV * 2;
+    static_assert(XCH_OFF + C::RWAVES * (NF + 2 * QB) * 64 * 4 <= C::LDS_BYTES, "exchange area fits the LDS");
+    float* xch = reinterpret_cast<float*>(smem + XCH_OFF) + rwave * (NF + 2 * QB) * 64;
+    if (kset == 1) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+        for (int db = 0; db < A::DB; ++db) {
+          agpr_fence<A::AG>(st.oacc[db][qb]);
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const f32x16& o = st.oacc[db][qb];
+            *reinterpret_cast<f32x4*>(xch + (((qb * A::DB + db) * 4 + g4) * 64 + lane) * 4) =
+                f32x4{o[4 * g4], o[4 * g4 + 1], o[4 * g4 + 2], o[4 * g4 + 3]};
+          }
+        }
+        xch[NF * 64 + qb * 64 + lane] = st.m_run[qb];
+        xch[NF * 64 + (QB + qb) * 64 + lane] = st.l_run[qb];
+      }
+    }
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    if (kset == 1) return;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const float m_b = xch[NF * 64 + qb * 64 + lane], l_b = xch[NF * 64 + (QB + qb) * 64 + lane];
+      const float m_a = st.m_run[qb], m = fmaxf(m_a, m_b);
+      const float wa = m_a == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_a - m);
+      const float wb = m_b == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_b - m);
+      st.m_run[qb] = m;
+      st.l_run[qb] = st.l_run[qb] * wa + l_b * wb;
+#pragma unroll
+      for (int db = 0; db < A::DB; ++db) {
+        agpr_fence<A::AG>(st.oacc[db][qb]);
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const f32x4 ob = *reinterpret_cast<const f32x4*>(xch + (((qb * A::DB + db) * 4 + g4) * 64 + lane) * 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) st.oacc[db][qb][4 * g4 + e] = st.oacc[db][qb][4 * g4 + e] * wa + ob[e] * wb;
+        }
+      }
+    }
+  }
 
   // ---- epilogue: O = acc / l, LSE = ln 2 * (m + log2 l) ---------------------------------------
   if constexpr (C::SPLIT) {
@@ -820,7 +888,7 @@ void fa_fwd_kernel_preload(const uint16_t* a_q, int a_sq, int a_sk, int a_hq, in
                             a_shifts});
 }
 
-// The two instances. Long: 4 waves x 64 query rows (256 row-heads per workgroup), one workgroup per CU,
+// The instances. Long: 4 waves x 64 query rows (256 row-heads per workgroup), one workgroup per CU,
 // one wave per SIMD; the register budget of a wave (O 128 + Q 64 AGPRs at d = 128, two score tiles
 // and P in VGPRs) is what fixes 64 query rows per wave. K tiles are loaded two ahead: a third K slot
 // measured 2-3 % slower on the 8K, 4K-d192 and 128K prefill shapes (one box, interleaved).
@@ -864,6 +932,16 @@ template <int DQK, int DV, bool CAUSAL>
 struct ShortInstance {
   using C = Cfg<DQK, DV, 64, 4, 1, CAUSAL, false, 2, DQK >= 128 ? 1 : 2, DQK >= 128 ? 2 : 6, 2, DQK >= 128 ? 3 : 4>;
 };
+// Key halves: 4 waves as two sets of 2 x 32 query rows (64 row-heads per workgroup), each set taking
+// one 32-key half of every tile; three workgroups per CU at d = 64 (three waves per SIMD, 132 VGPRs,
+// 48 KiB of LDS each), two at d = 128 (208 VGPRs, 80 KiB). It runs problems whose grid of long-
+// instance blocks is small enough that each workgroup's chain of steps sets the time: the chain
+// keeps its number of steps but each step carries half the work per wave. V fragments are read 4
+// ahead at d = 64 and 2 at d = 128, the best of 2-8 measured (one box, interleaved).
+template <int DQK, int DV, bool CAUSAL>
+struct HalfInstance {
+  using C = Cfg<DQK, DV, 64, 4, 1, CAUSAL, false, DQK >= 128 ? 2 : 3, 2, DQK >= 128 ? 2 : 4, 2, DQK >= 128 ? 3 : 4, 2>;
+};
 
 // Largest grid of long-instance blocks (256 row-heads) that runs the short instance instead. At
 // d = 128 the CU count of MI355X, where the long instance would leave CUs idle. At d = 64, where a
@@ -872,12 +950,21 @@ struct ShortInstance {
 // causal and non-causal GPT-2-shaped problems of 384-768 blocks, level at 1024-1152, 3-4 % slower from
 // 1536 blocks on (one box, interleaved).
 constexpr int64_t kShortMaxBlocks64 = 1024, kShortMaxBlocks128 = 256;
+// Largest grid of such blocks that runs the key-halves instance, by head dimension and masking.
+// Causal problems have a longest chain of steps (the last query block's) that halving each step's
+// work per wave shortens; problems without a mask gain only while the grid leaves SIMDs idle.
+constexpr int64_t kHalfMaxCausal64 = 320, kHalfMaxFull64 = 64, kHalfMaxCausal128 = 256, kHalfMaxFull128 = 128;
 
-bool use_short(const FwdParams& p, int d_qk, int d_v) {
-  if (!((d_qk == 64 && d_v == 64) || (d_qk == 128 && d_v == 128))) return false;
+enum class Kind { kLong, kShort, kHalf };
+
+Kind pick_instance(const FwdParams& p, int d_qk, int d_v, bool causal) {
+  if (!((d_qk == 64 && d_v == 64) || (d_qk == 128 && d_v == 128))) return Kind::kLong;
   const int bm = Instance<64, 64, false>::C::BM;
   const int64_t blocks = (int64_t)p.batch * p.hq * ((p.sq + bm - 1) / bm);
-  return blocks <= (d_qk == 64 ? kShortMaxBlocks64 : kShortMaxBlocks128);
+  const int64_t half_max = d_qk == 64 ? (causal ? kHalfMaxCausal64 : kHalfMaxFull64)
+                                      : (causal ? kHalfMaxCausal128 : kHalfMaxFull128);
+  if (blocks <= half_max) return Kind::kHalf;
+  return blocks <= (d_qk == 64 ? kShortMaxBlocks64 : kShortMaxBlocks128) ? Kind::kShort : Kind::kLong;
 }
 
 // log2 of the query heads a workgroup of `nwaves` waves packs: 4, 2 or 1 heads, the largest that
@@ -890,9 +977,9 @@ int packed_heads_log2(int group, int nwaves) {
 
 template <class C>
 hipError_t launch_cfg(FwdParams p, hipStream_t stream) {
-  const int hw_log = packed_heads_log2(p.group, C::NWAVES);
+  const int hw_log = packed_heads_log2(p.group, C::RWAVES);
   const int gi = p.group >> hw_log;  // workgroups per key/value head and query block
-  const int bmr = (C::NWAVES >> hw_log) * 32 * C::QB;
+  const int bmr = (C::RWAVES >> hw_log) * 32 * C::QB;
   p.n_qtiles = (p.sq + bmr - 1) / bmr;
   p.n_wg = p.batch * p.hkv * gi * p.n_qtiles;
   const int span = kNumXcd * gi;
@@ -915,16 +1002,19 @@ hipError_t launch_cfg(FwdParams p, hipStream_t stream) {
 }
 
 template <int DQK, int DV, bool CAUSAL, bool SPLIT>
-hipError_t launch_instance(FwdParams p, bool short_blocks, hipStream_t stream) {
+hipError_t launch_instance(FwdParams p, Kind kind, hipStream_t stream) {
   if constexpr (!SPLIT && DQK != 192) {
-    if (short_blocks) return launch_cfg<typename ShortInstance<DQK, DV, CAUSAL>::C>(p, stream);
+    if (kind == Kind::kHalf) return launch_cfg<typename HalfInstance<DQK, DV, CAUSAL>::C>(p, stream);
+  }
+  if constexpr (!SPLIT && DQK != 192) {
+    if (kind == Kind::kShort) return launch_cfg<typename ShortInstance<DQK, DV, CAUSAL>::C>(p, stream);
   }
   return launch_cfg<typename Instance<DQK, DV, CAUSAL, SPLIT>::C>(p, stream);
 }
 
 template <bool SPLIT>
 hipError_t launch_dims(FwdParams p, int d_qk, int d_v, bool causal, hipStream_t stream) {
-  const bool sh = !SPLIT && use_short(p, d_qk, d_v);
+  const Kind sh = SPLIT ? Kind::kLong : pick_instance(p, d_qk, d_v, causal);
   if (d_qk == 64 && d_v == 64)
     return causal ? launch_instance<64, 64, true, SPLIT>(p, sh, stream)
                   : launch_instance<64, 64, false, SPLIT>(p, sh, stream);
@@ -1001,10 +1091,27 @@ int block_rows(int d_qk, int d_v, bool causal) {
   return 0;
 }
 
+int instance_rows(int batch, int hq, int sq, int d_qk, int d_v, bool causal) {
+  const int bm = block_rows(d_qk, d_v, causal);
+  if (bm == 0 || batch < 0 || hq < 0 || sq < 0) return 0;
+  FwdParams p{};
+  p.batch = batch;
+  p.hq = hq;
+  p.sq = sq;
+  switch (pick_instance(p, d_qk, d_v, causal)) {
+    case Kind::kHalf:
+      return HalfInstance<64, 64, false>::C::BM;
+    case Kind::kShort:
+      return ShortInstance<64, 64, false>::C::BM;
+    default:
+      return bm;
+  }
+}
+
 int64_t forward_workgroups(int batch, int hq, int hkv, int sq) {
-  // the long instance's grid (the short instance runs only grids of at most 512 workgroups)
+  // the long instance's grid (the other instances run only grids of at most 2 048 workgroups)
   using C = Instance<64, 64, false>::C;
-  const int group = hq / hkv, hw_log = packed_heads_log2(group, C::NWAVES);
+  const int group = hq / hkv, hw_log = packed_heads_log2(group, C::RWAVES);
   const int64_t bmr = (C::NWAVES >> hw_log) * 32 * C::QB;
   return (int64_t)batch * hkv * (group >> hw_log) * ((sq + bmr - 1) / bmr);
 }

@@ -44,12 +44,15 @@ struct MergeParams {
 };
 
 // Query rows per workgroup of the long kernel instance for (d_qk, d_v, causal) when a workgroup holds
-// one query head (split mode, and problems with more such blocks than the short instance takes); 0 if
-// not compiled in.
+// one query head (split mode, every d_qk = 192 problem, and problems with more such blocks than the
+// other instances take); 0 if not compiled in.
 // With a GQA group size divisible by 2 or 4 a workgroup holds as many query heads, each with half or
-// a quarter of these rows. Problems with at most 1024 blocks at d = 64 or 256 at d = 128 run the
-// short instance, with half as many rows per workgroup.
+// a quarter of these rows.
 int block_rows(int d_qk, int d_v, bool causal);
+// Query rows per workgroup holding one query head of the instance the fused forward runs for this
+// problem: the long instance's block_rows() (256), the short instance's 128 or the key-halves
+// instance's 64; 0 for unsupported head dimensions or negative sizes.
+int instance_rows(int batch, int hq, int sq, int d_qk, int d_v, bool causal);
 // Workgroups of the long instance's grid (one part per query block and packed heads).
 int64_t forward_workgroups(int batch, int hq, int hkv, int sq);
 

@@ -68,6 +68,32 @@ def test_block_rows(lib):
     assert fa.fa_block_rows(128, 64, False) == 0
 
 
+def _fwd_rows_expected(blocks, d, causal):
+    """The dispatch fa.h states for (d, d) problems of `blocks` 256-row blocks."""
+    half = (320 if causal else 64) if d == 64 else (256 if causal else 128)
+    short = 1024 if d == 64 else 256
+    return 64 if blocks <= half else 128 if blocks <= short else 256
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_fwd_rows_follows_the_grid(lib, d, causal):
+    # B * Hq * ceil(Sq / 256) blocks, reached through each of the three factors, on both sides of
+    # every switch
+    for blocks in (1, 2, 63, 64, 65, 128, 129, 255, 256, 257, 320, 321, 1024, 1025, 5000):
+        for B, Hq, Sq in ((blocks, 1, 256), (1, blocks, 200), (1, 1, 256 * blocks - 255)):
+            assert fa.fa_fwd_rows(B, Hq, Sq, d, d, causal) == _fwd_rows_expected(blocks, d, causal), (B, Hq, Sq)
+    assert fa.fa_fwd_rows(0, 8, 100, d, d, causal) in (64, 128, 256)
+
+
+def test_fwd_rows_other_dims(lib):
+    assert fa.fa_fwd_rows(1, 1, 64, 192, 128, True) == fa.fa_block_rows(192, 128, True) == 256
+    assert fa.fa_fwd_rows(1, 1, 64, 96, 96, True) == 0
+    assert fa.fa_fwd_rows(1, 1, 64, 128, 64, False) == 0
+    assert fa.fa_fwd_rows(-1, 1, 64, 64, 64, False) == 0
+    assert fa.fa_fwd_rows(1, 1, -64, 64, 64, False) == 0
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(B=-1), fa.FA_ERR_BAD_SHAPE),
     (dict(Hq=-4), fa.FA_ERR_BAD_SHAPE),

@@ -19,9 +19,12 @@ pytestmark = pytest.mark.gpu
 
 # name: (B, Hq, Hkv, Sq, Sk, d_qk, d_v, causal, call)
 CASES = {
+    # a few query blocks: the key-halves instance
     "fused": (1, 4, 2, 300, 300, 128, 128, True, lambda q, k, v, c: fa.forward(q, k, v, causal=c, return_lse=True)),
-    # more than 256 query blocks of 256 rows at d = 128: the long instance (the case above runs the
-    # short one)
+    # 96 blocks of 256 rows at d = 64 without a mask: the short instance
+    "fused-short": (1, 96, 48, 130, 200, 64, 64, False,
+                    lambda q, k, v, c: fa.forward(q, k, v, causal=c, return_lse=True)),
+    # more than 256 blocks at d = 128: the long instance
     "fused-long": (1, 264, 66, 130, 200, 128, 128, False,
                    lambda q, k, v, c: fa.forward(q, k, v, causal=c, return_lse=True)),
     "fused-d192": (2, 2, 1, 130, 200, 192, 128, False,
@@ -42,9 +45,15 @@ def inputs(case, seed):
     return W.make_inputs(w)
 
 
+INSTANCE = {"fused": 64, "fused-short": 128, "fused-long": 256, "fused-d192": 256}
+
+
 @pytest.mark.parametrize("case", list(CASES))
 def test_graph_replay_matches_eager(case):
     causal, call = CASES[case][7], CASES[case][8]
+    if case in INSTANCE:
+        B, Hq, _, Sq, _, dqk, dv, _, _ = CASES[case]
+        assert fa.fa_fwd_rows(B, Hq, Sq, dqk, dv, causal) == INSTANCE[case]
     sets = [inputs(case, 7100), inputs(case, 7200)]
     q, k, v = (t.cuda() for t in sets[0])
 

@@ -1,11 +1,12 @@
-"""GPU parity of both instances of the fused kernel.
+"""GPU parity of the three instances of the fused kernel.
 
-Problems with at most 1024 (d = 64) or 256 (d = 128) query blocks of fa_block_rows() rows
-(B * Hq * ceil(Sq / rows)) at (d_qk, d_v) = (64, 64) or (128, 128) run the short instance (half as
-many rows per workgroup, two workgroups per CU); every other problem runs the long instance. The
-small edge cases of test_gpu_parity.py have few blocks and so exercise the short instance; here the
-same cases are widened past the switch (more heads, same per-head shape and GQA ratio, seeded afresh)
-so that the long instance meets them too, and every output element is compared with the fp64 oracle.
+Which instance runs follows from the grid alone, and the library reports it (fa_fwd_rows, the query
+rows of one head per workgroup): the key-halves instance (64) for the smallest grids, the short
+instance (128) for mid-sized ones at d = 64 and, without a mask, at d = 128, and the long instance
+(256) for the rest and for every d_qk = 192 problem. The small edge cases of test_gpu_parity.py have
+few blocks, so they run the instance of the smallest grids; here the same cases are widened (more
+heads, same per-head shape and GQA ratio, seeded afresh) until each other instance runs them, and
+every output element is compared with the fp64 oracle.
 """
 
 import numpy as np
@@ -20,48 +21,79 @@ from test_gpu_parity import SMALL_CASES
 
 pytestmark = pytest.mark.gpu
 
-SHORT_MAX = {64: 1024, 128: 256}  # largest block count that runs the short instance, by head dim
+HALF, SHORT, LONG = 64, 128, 256  # rows per workgroup of one head, by instance
+NAMES = {HALF: "halves", SHORT: "short", LONG: "long"}
+
+
+def rows(w):
+    return fa.fa_fwd_rows(w.B, w.Hq, w.Sq, w.dqk, w.dv, w.causal)
 
 
 def blocks(w):
-    bm = fa.fa_block_rows(w.dqk, w.dv, w.causal)
-    return w.B * w.Hq * -(-w.Sq // bm)
+    return w.B * w.Hq * -(-w.Sq // fa.fa_block_rows(w.dqk, w.dv, w.causal))
 
 
-def short(w):
-    return w.dqk == w.dv and w.dqk in SHORT_MAX and blocks(w) <= SHORT_MAX[w.dqk]
+def widened(w, target):
+    """The same per-head problem with the fewest multiples of its heads that run the instance of
+    `target` rows, or None if no head count does (the instances follow each other as the grid grows:
+    key halves, short, long)."""
+    for m in range(1, 8192):
+        v = w.with_(Hq=w.Hq * m, Hkv=w.Hkv * m)
+        r = rows(v)
+        if r == target:
+            return v.with_(name=w.name + f" x{m} heads", seed=w.seed + 500 + target)
+        if r > target:
+            return None
+    return None
 
 
-def widened(w):
-    """The same per-head problem with enough heads for the long instance."""
-    m = -(-(SHORT_MAX[w.dqk] + 1) // blocks(w))
-    v = w.with_(name=w.name + f" x{m} heads", Hq=w.Hq * m, Hkv=w.Hkv * m, seed=w.seed + 500)
-    assert not short(v)
-    return v
+def has_short(d, causal):
+    """Causal problems at d = 128 go from the key-halves instance straight to the long one."""
+    return not (d == 128 and causal)
 
 
 CASES = [w for w in SMALL_CASES if (w.dqk, w.dv) != (192, 128)]
+WIDE = [(w, t) for w in CASES for t in (SHORT, LONG) if t != SHORT or has_short(w.dqk, w.causal)]
 
 
-def test_small_cases_run_the_short_instance():
+def test_small_cases_run_the_key_halves_instance():
     # the premise of this file: the edge cases of test_gpu_parity.py have few blocks
-    assert CASES and all(short(w) for w in CASES)
+    assert CASES and all(rows(w) == HALF for w in CASES)
+    assert all(rows(w) == LONG for w in SMALL_CASES if w.dqk == 192)
+    # and the cases left out below have no short instance to widen to
+    assert all(widened(w, SHORT) is None for w in CASES if not has_short(w.dqk, w.causal))
 
 
-@pytest.mark.parametrize("w", CASES, ids=[c.name for c in CASES])
-def test_long_instance_small_shapes_match_oracle(w):
-    v = widened(w)
+@pytest.mark.parametrize("w,target", WIDE, ids=[f"{w.name}-{NAMES[t]}" for w, t in WIDE])
+def test_wider_instances_small_shapes_match_oracle(w, target):
+    v = widened(w, target)
     print(f"\n[case] {v}", flush=True)
     check_full(v)
 
 
-@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
-@pytest.mark.parametrize("heads", [2, 2 * 43], ids=["short", "long"])
-def test_rising_maxima_rebase_both_instances(causal, heads):
+def _heads_for(make, target):
+    """The smallest even head count whose problem `make(heads)` runs the instance of `target` rows."""
+    for heads in range(2, 8192, 2):
+        r = rows(make(heads))
+        if r == target:
+            return heads
+        if r > target:
+            return None
+    return None
+
+
+SPIKES = [(c, t) for c in (False, True) for t in (HALF, SHORT, LONG) if t != SHORT or has_short(128, c)]
+
+
+@pytest.mark.parametrize("causal,target", SPIKES,
+                         ids=[f"{'causal' if c else 'full'}-{NAMES[t]}" for c, t in SPIKES])
+def test_rising_maxima_rebase_every_instance(causal, target):
     """Keys whose scores jump far above everything before them in the second key tile, two middle
     tiles and the last one, so that tiles are redone from their exact maximum at each position."""
-    w = W.small("spikes", dqk=128, dv=128, Hq=heads, Hkv=heads // 2, Sq=640, Sk=640, causal=causal, seed=181)
-    assert short(w) == (heads == 2)
+    make = lambda heads: W.small("spikes", dqk=128, dv=128, Hq=heads, Hkv=heads // 2, Sq=640, Sk=640,
+                                 causal=causal, seed=181)
+    heads = _heads_for(make, target)
+    w = make(heads)
     q, k, v = W.make_inputs(w)
     for key, factor in ((70, 4.0), (300, 8.0), (520, 16.0), (600, 32.0)):
         k[:, :, key] *= factor
@@ -72,12 +104,16 @@ def test_rising_maxima_rebase_both_instances(causal, heads):
     compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name)
 
 
-@pytest.mark.parametrize("mult", [1, 0], ids=["short", "long"])
-@pytest.mark.parametrize("d", [64, 128])
-def test_causal_first_row_bitwise_both_instances(mult, d):
-    heads = 4 if mult else 2 * (SHORT_MAX[d] // 4 + 1)  # 300 rows: 2 blocks per head
-    w = W.small("row0", dqk=d, dv=d, Hq=heads, Hkv=heads // 2, Sq=300, Sk=300, causal=True, seed=151)
-    assert short(w) == bool(mult)
+ROW0 = [(d, t) for d in (64, 128) for t in (HALF, SHORT, LONG) if t != SHORT or has_short(d, True)]
+
+
+@pytest.mark.parametrize("d,target", ROW0, ids=[f"d{d}-{NAMES[t]}" for d, t in ROW0])
+def test_causal_first_row_bitwise_every_instance(d, target):
+    # 300 rows: 2 blocks per head; row 0 sees key 0 only, so its output is V's row 0 bit for bit
+    make = lambda heads: W.small("row0", dqk=d, dv=d, Hq=heads, Hkv=heads // 2, Sq=300, Sk=300, causal=True,
+                                 seed=151)
+    heads = _heads_for(make, target)
+    w = make(heads)
     q, k, v = W.make_inputs(w)
     o, _ = run_gpu(q, k, v, w)
     o = o.cpu()
@@ -86,19 +122,29 @@ def test_causal_first_row_bitwise_both_instances(mult, d):
 
 
 @pytest.mark.parametrize("cfg", [1, 2])
-def test_short_instance_runs_the_small_benchmark_configs(cfg):
-    # configs 1 (one block) and 2 (192 blocks) run the short instance; test_gpu_parity checks them
-    # in full, and here on a second seed
+def test_small_benchmark_configs_second_seed(cfg):
+    # configs 1 (one block: key halves) and 2 (384 blocks: short); test_gpu_parity checks them in
+    # full, and here on a second seed
     w = W.CONFIGS[cfg]
-    assert short(w)
+    assert rows(w) == (HALF if cfg == 1 else SHORT)
     check_full(w.with_(seed=w.seed + 700))
 
 
-@pytest.mark.parametrize("d,heads", [(128, 256), (128, 257), (64, 1024), (64, 1025)],
-                         ids=["d128-256-short", "d128-257-long", "d64-1024-short", "d64-1025-long"])
-def test_instance_boundary(d, heads):
-    """Either side of the switch between the instances at each head dimension."""
-    w = W.small(f"boundary d{d} {heads}", dqk=d, dv=d, Hq=heads, Hkv=heads, Sq=100, Sk=150, causal=True, seed=191)
-    assert blocks(w) == heads and short(w) == (heads == SHORT_MAX[d])
-    print(f"\n[case] {w}", flush=True)
+# (d, causal, B * Hq * ceil(Sq / 256)) of the last grid before each switch between the instances
+SWITCHES = [(64, True, 320), (64, True, 1024), (64, False, 64), (64, False, 1024), (128, True, 256),
+            (128, False, 128), (128, False, 256)]
+BOUNDARY = [(d, c, n + side) for d, c, n in SWITCHES for side in (0, 1)]
+
+
+@pytest.mark.parametrize("d,causal,heads", BOUNDARY,
+                         ids=[f"d{d}-{'causal' if c else 'full'}-{h}" for d, c, h in BOUNDARY])
+def test_instance_boundary(d, causal, heads):
+    """Either side of each switch between the instances; one block per head (Sq = 100)."""
+    make = lambda n: W.small(f"boundary d{d} {n}", dqk=d, dv=d, Hq=n, Hkv=n, Sq=100, Sk=150, causal=causal,
+                             seed=191)
+    w = make(heads)
+    assert blocks(w) == heads
+    last = heads if (d, causal, heads) in SWITCHES else heads - 1
+    assert rows(make(last + 1)) > rows(make(last))
+    print(f"\n[case] {w} ({NAMES[rows(w)]})", flush=True)
     check_full(w)

@@ -7,8 +7,9 @@ every head), K = 0 except the last key K[L] = (s_h / scale) e0 with a score s_h 
 key/value head h, V = a except V[L] = b. A query row that sees the keys 0 .. n-1 (n <= L) gets O = a
 and LSE = ln n; a row that also sees key L gets O = (L a + e^s b) / (L + e^s) and LSE = ln(L + e^s).
 The last key's score sits far above the others, so the fused kernel's online softmax must rebase on
-the last tile. Two query heads share each key/value head (grouped-query attention); a second fused
-run with 129 per key/value head has enough query blocks for the long kernel instance.
+the last tile. Two query heads share each key/value head (grouped-query attention), which runs the
+key-halves kernel instance; further fused runs with 100 and 129 per key/value head have enough query
+blocks for the short (without a mask) and the long instance.
 """
 
 import math
@@ -77,6 +78,7 @@ def big():
 @pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
 def test_fused_at_largest_key_length(big, causal):
     sq, q, k, v = big
+    assert fa.fa_fwd_rows(1, q.shape[1], sq, D, D, causal) == 64
     o, lse = fa.forward(q, k, v, causal=causal, scale=SCALE, return_lse=True)
     torch.cuda.synchronize()
     check(o, lse, sq, MAX_SK, causal, f"fused causal={causal}")
@@ -84,16 +86,29 @@ def test_fused_at_largest_key_length(big, causal):
 
 @pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
 def test_fused_long_instance_at_largest_key_length(big, causal):
-    """The same keys with 129 query heads per key/value head: 258 query blocks, more than the short
-    instance takes, so the long instance's loaders address the end of the 4 GiB heads."""
+    """The same keys with 129 query heads per key/value head: 258 query blocks, more than the other
+    instances take, so the long instance's loaders address the end of the 4 GiB heads."""
     sq, _, k, v = big
     group = 129
-    assert 2 * group * -(-sq // fa.fa_block_rows(D, D, causal)) > 256
+    assert fa.fa_fwd_rows(1, 2 * group, sq, D, D, causal) == 256
     q = torch.zeros(1, 2 * group, sq, D, dtype=torch.bfloat16, device="cuda")
     q[..., 0] = 1.0
     o, lse = fa.forward(q, k, v, causal=causal, scale=SCALE, return_lse=True)
     torch.cuda.synchronize()
     check(o, lse, sq, MAX_SK, causal, f"fused long causal={causal}", group)
+
+
+def test_fused_short_instance_at_largest_key_length(big):
+    """100 query heads per key/value head without a mask: 200 query blocks, which the short instance
+    runs (causal problems at this head dimension go from the key-halves to the long instance)."""
+    sq, _, k, v = big
+    group = 100
+    assert fa.fa_fwd_rows(1, 2 * group, sq, D, D, False) == 128
+    q = torch.zeros(1, 2 * group, sq, D, dtype=torch.bfloat16, device="cuda")
+    q[..., 0] = 1.0
+    o, lse = fa.forward(q, k, v, causal=False, scale=SCALE, return_lse=True)
+    torch.cuda.synchronize()
+    check(o, lse, sq, MAX_SK, False, "fused short", group)
 
 
 def test_split_at_largest_key_length(big):

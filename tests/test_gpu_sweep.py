@@ -5,7 +5,8 @@ The hand-picked edge cases of the other GPU test files cover what each code path
 on; this file draws many more combinations of the same parameters at once (head dimensions, GQA
 group size, batch, ragged query and key lengths, causal masking, scale and input spread) from a fixed
 seed, so that an interaction nobody thought of still meets the oracle. A quarter of the fused cases
-carry enough heads for the long instance, so both kernel instances are drawn.
+carry enough heads for the long kernel instance and a fifth enough for the short one (where the head
+dimension and mask have one); the rest are small grids, which run the key-halves instance.
 """
 
 import numpy as np
@@ -20,7 +21,10 @@ from parity import compare, rounding_bar, to_f64
 pytestmark = pytest.mark.gpu
 
 DIMS = [(64, 64), (128, 128), (192, 128)]
-SHORT_MAX = {64: 1024, 128: 256}  # largest block count (256 rows) that runs the short instance
+# largest grid of 256-row blocks that runs the short instance (by d_qk) and the key-halves instance
+# (by d_qk and causal masking), as fa_fwd_rows reports; checked against it below
+SHORT_MAX = {64: 1024, 128: 256}
+HALF_MAX = {(64, True): 320, (64, False): 64, (128, True): 256, (128, False): 128}
 GROUPS = [1, 2, 3, 4, 7, 8]
 
 
@@ -42,10 +46,12 @@ def _draw(rng, idx, kind):
     else:
         sq = _length(rng, 1, 700)
         sk = sq if rng.uniform() < 0.4 else _length(rng, 1, 700)
-        if rng.uniform() < 0.25:  # past the short instance's largest grid: the long instance
+        u = rng.uniform()
+        if u < 0.45:  # past the key-halves (u >= 0.25) or the short instance's (u < 0.25) largest grid
             sq = min(sq, 300)
             sk = min(sk, 300)
-            b, hkv = 1, -(-(SHORT_MAX.get(dqk, 256) + 1) // (g * -(-sq // 256)))
+            top = SHORT_MAX.get(dqk, 256) if u < 0.25 else HALF_MAX.get((dqk, causal), 0)
+            b, hkv = 1, -(-(top + 1) // (g * -(-sq // 256)))
     scale = None if rng.uniform() < 0.7 else float(rng.uniform(-0.3, 0.5))
     sigma = float(rng.choice([1.0, 1.0, 0.5, 2.0]))
     seed = 5000 + 100 * ["fused", "split", "decode"].index(kind) + idx
@@ -78,11 +84,18 @@ def _check(w, **kw):
     compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name, max(1.0, w.sigma), o_bar=bar)
 
 
-def test_sweep_draws_both_instances_and_every_head_dimension():
-    blocks = [w.B * w.Hq * -(-w.Sq // fa.fa_block_rows(w.dqk, w.dv, w.causal)) for w in FUSED]
-    short = [w.dqk in SHORT_MAX and n <= SHORT_MAX[w.dqk] for w, n in zip(FUSED, blocks)]
-    assert any(short) and not all(short)
-    assert any(not s and w.dqk == 64 for s, w in zip(short, FUSED))
+def _rows_model(w):
+    blocks = w.B * w.Hq * -(-w.Sq // 256)
+    if w.dqk == 192:
+        return 256
+    return 64 if blocks <= HALF_MAX[(w.dqk, w.causal)] else 128 if blocks <= SHORT_MAX[w.dqk] else 256
+
+
+def test_sweep_draws_every_instance_and_head_dimension():
+    rows = [fa.fa_fwd_rows(w.B, w.Hq, w.Sq, w.dqk, w.dv, w.causal) for w in FUSED]
+    assert rows == [_rows_model(w) for w in FUSED]
+    for d in (64, 128):
+        assert {r for r, w in zip(rows, FUSED) if w.dqk == d} == {64, 128, 256}
     assert {(w.dqk, w.dv) for w in FUSED} == set(DIMS)
     assert len(DECODE) == 48 and all(w.Sq <= 20 for w in DECODE)
 
