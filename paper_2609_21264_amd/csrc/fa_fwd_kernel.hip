@@ -542,7 +542,7 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   // With key halves (KSPLIT = 2) the same applies within each wave set: wave w belongs to set
   // w / RWAVES, which takes keys [kpart, kpart + WBN) of every tile, and to row chunk w % RWAVES.
   const int hw_log = (int)((wm.shifts >> 18) & 3u);
-  const int kset = wave / C::RWAVES, rwave = wave % C::RWAVES;
+  const int kset = C::KSPLIT > 1 ? wave / C::RWAVES : 0, rwave = C::KSPLIT > 1 ? wave % C::RWAVES : wave;
   const int kpart = kset * C::WBN;                       // first key of this wave's part of a tile
   const int rw = C::RWAVES >> hw_log;                    // row chunks per head
   const int bmr = rw * 32 * QB;                          // query rows of the block
