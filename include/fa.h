@@ -286,7 +286,7 @@ int fa_block_rows(int d_qk, int d_v, int causal);
  * 256 (long instance: one workgroup per compute unit), 128 (short instance: two per compute unit, at
  * most 1024 blocks at d = 64 and 256 at d = 128, i.e. blocks of the long instance's rows) or 64 (key
  * halves: each half of a workgroup's waves takes one half of every key tile, and the halves are
- * merged at the end; causal problems of at most 320 blocks at d = 64 and 256 at d = 128, others of at
+ * merged at the end; causal problems of at most 320 blocks at d = 64 and 192 at d = 128, others of at
  * most 64 and 128). Every instance computes the same function (Eq. (1) by Alg. 1); which one runs
  * follows from the grid size alone. 0 for unsupported head dimensions or negative sizes. Host
  * arithmetic only. */

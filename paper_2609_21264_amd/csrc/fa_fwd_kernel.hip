@@ -952,8 +952,10 @@ struct HalfInstance {
 constexpr int64_t kShortMaxBlocks64 = 1024, kShortMaxBlocks128 = 256;
 // Largest grid of such blocks that runs the key-halves instance, by head dimension and masking.
 // Causal problems have a longest chain of steps (the last query block's) that halving each step's
-// work per wave shortens; problems without a mask gain only while the grid leaves SIMDs idle.
-constexpr int64_t kHalfMaxCausal64 = 320, kHalfMaxFull64 = 64, kHalfMaxCausal128 = 256, kHalfMaxFull128 = 128;
+// work per wave shortens; problems without a mask gain only while the grid leaves SIMDs idle. At
+// d = 128 causal grids of 256 blocks measured 0.96-1.06x against the short instance (the paper's
+// Llama S = 2048 shapes on the slow side), so they stay with it.
+constexpr int64_t kHalfMaxCausal64 = 320, kHalfMaxFull64 = 64, kHalfMaxCausal128 = 192, kHalfMaxFull128 = 128;
 
 enum class Kind { kLong, kShort, kHalf };
 

@@ -70,7 +70,7 @@ def test_block_rows(lib):
 
 def _fwd_rows_expected(blocks, d, causal):
     """The dispatch fa.h states for (d, d) problems of `blocks` 256-row blocks."""
-    half = (320 if causal else 64) if d == 64 else (256 if causal else 128)
+    half = (320 if causal else 64) if d == 64 else (192 if causal else 128)
     short = 1024 if d == 64 else 256
     return 64 if blocks <= half else 128 if blocks <= short else 256
 
@@ -80,7 +80,7 @@ def _fwd_rows_expected(blocks, d, causal):
 def test_fwd_rows_follows_the_grid(lib, d, causal):
     # B * Hq * ceil(Sq / 256) blocks, reached through each of the three factors, on both sides of
     # every switch
-    for blocks in (1, 2, 63, 64, 65, 128, 129, 255, 256, 257, 320, 321, 1024, 1025, 5000):
+    for blocks in (1, 2, 63, 64, 65, 128, 129, 192, 193, 255, 256, 257, 320, 321, 1024, 1025, 5000):
         for B, Hq, Sq in ((blocks, 1, 256), (1, blocks, 200), (1, 1, 256 * blocks - 255)):
             assert fa.fa_fwd_rows(B, Hq, Sq, d, d, causal) == _fwd_rows_expected(blocks, d, causal), (B, Hq, Sq)
     assert fa.fa_fwd_rows(0, 8, 100, d, d, causal) in (64, 128, 256)

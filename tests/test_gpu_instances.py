@@ -2,8 +2,8 @@
 
 Which instance runs follows from the grid alone, and the library reports it (fa_fwd_rows, the query
 rows of one head per workgroup): the key-halves instance (64) for the smallest grids, the short
-instance (128) for mid-sized ones at d = 64 and, without a mask, at d = 128, and the long instance
-(256) for the rest and for every d_qk = 192 problem. The small edge cases of test_gpu_parity.py have
+instance (128) for mid-sized ones, and the long instance (256) for the rest and for every
+d_qk = 192 problem. The small edge cases of test_gpu_parity.py have
 few blocks, so they run the instance of the smallest grids; here the same cases are widened (more
 heads, same per-head shape and GQA ratio, seeded afresh) until each other instance runs them, and
 every output element is compared with the fp64 oracle.
@@ -47,21 +47,14 @@ def widened(w, target):
     return None
 
 
-def has_short(d, causal):
-    """Causal problems at d = 128 go from the key-halves instance straight to the long one."""
-    return not (d == 128 and causal)
-
-
 CASES = [w for w in SMALL_CASES if (w.dqk, w.dv) != (192, 128)]
-WIDE = [(w, t) for w in CASES for t in (SHORT, LONG) if t != SHORT or has_short(w.dqk, w.causal)]
+WIDE = [(w, t) for w in CASES for t in (SHORT, LONG)]
 
 
 def test_small_cases_run_the_key_halves_instance():
     # the premise of this file: the edge cases of test_gpu_parity.py have few blocks
     assert CASES and all(rows(w) == HALF for w in CASES)
     assert all(rows(w) == LONG for w in SMALL_CASES if w.dqk == 192)
-    # and the cases left out below have no short instance to widen to
-    assert all(widened(w, SHORT) is None for w in CASES if not has_short(w.dqk, w.causal))
 
 
 @pytest.mark.parametrize("w,target", WIDE, ids=[f"{w.name}-{NAMES[t]}" for w, t in WIDE])
@@ -82,7 +75,7 @@ def _heads_for(make, target):
     return None
 
 
-SPIKES = [(c, t) for c in (False, True) for t in (HALF, SHORT, LONG) if t != SHORT or has_short(128, c)]
+SPIKES = [(c, t) for c in (False, True) for t in (HALF, SHORT, LONG)]
 
 
 @pytest.mark.parametrize("causal,target", SPIKES,
@@ -104,7 +97,7 @@ def test_rising_maxima_rebase_every_instance(causal, target):
     compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name)
 
 
-ROW0 = [(d, t) for d in (64, 128) for t in (HALF, SHORT, LONG) if t != SHORT or has_short(d, True)]
+ROW0 = [(d, t) for d in (64, 128) for t in (HALF, SHORT, LONG)]
 
 
 @pytest.mark.parametrize("d,target", ROW0, ids=[f"d{d}-{NAMES[t]}" for d, t in ROW0])
@@ -131,7 +124,7 @@ def test_small_benchmark_configs_second_seed(cfg):
 
 
 # (d, causal, B * Hq * ceil(Sq / 256)) of the last grid before each switch between the instances
-SWITCHES = [(64, True, 320), (64, True, 1024), (64, False, 64), (64, False, 1024), (128, True, 256),
+SWITCHES = [(64, True, 320), (64, True, 1024), (64, False, 64), (64, False, 1024), (128, True, 192), (128, True, 256),
             (128, False, 128), (128, False, 256)]
 BOUNDARY = [(d, c, n + side) for d, c, n in SWITCHES for side in (0, 1)]
 

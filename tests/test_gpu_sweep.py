@@ -24,7 +24,7 @@ DIMS = [(64, 64), (128, 128), (192, 128)]
 # largest grid of 256-row blocks that runs the short instance (by d_qk) and the key-halves instance
 # (by d_qk and causal masking), as fa_fwd_rows reports; checked against it below
 SHORT_MAX = {64: 1024, 128: 256}
-HALF_MAX = {(64, True): 320, (64, False): 64, (128, True): 256, (128, False): 128}
+HALF_MAX = {(64, True): 320, (64, False): 64, (128, True): 192, (128, False): 128}
 GROUPS = [1, 2, 3, 4, 7, 8]
 
 
