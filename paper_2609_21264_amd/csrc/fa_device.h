@@ -129,6 +129,24 @@ struct TileLoader {
     const uint32_t left = (int)rows > n0 ? (rows - (uint32_t)n0) * kRowBytes : 0u;
     return u32x4{(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, left, 0x00020000u};
   }
+  // Walking the tiles in order: rsrc_walk(n0, rem) is rsrc(n0) with rem = rows - n0 (signed, may be
+  // negative), and advance() moves both on by BN rows. The base's high word gains only the carry (a
+  // device address stays below 2^48, so the stride field above bit 16 stays 0), and the bytes left
+  // are max(rem, 0) rows: scalar add, add-with-carry, max and shift, where rsrc() multiplies and
+  // compares. A saturating unsigned subtract instead would be selected as a vector instruction, and
+  // the descriptor must stay in scalar registers.
+  __device__ __forceinline__ u32x4 rsrc_walk(int n0, int& rem) const {
+    rem = (int)rows - n0;
+    return rsrc(n0);
+  }
+  __device__ __forceinline__ void advance(u32x4& r, int& rem) const {
+    constexpr uint32_t kStep = BN * kRowBytes;
+    const uint64_t base = (((uint64_t)r.y << 32) | r.x) + kStep;
+    r.x = (uint32_t)base;
+    r.y = (uint32_t)(base >> 32);
+    rem -= BN;
+    r.z = (uint32_t)max(rem, 0) * kRowBytes;
+  }
   __device__ __forceinline__ uint32_t lds(unsigned char* slot, int wave) const {
     return lds_offset(slot + wave * NI * 1024);
   }

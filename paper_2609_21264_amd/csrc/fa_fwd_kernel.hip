@@ -597,8 +597,9 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   TileLoader<C::NWAVES, BN, C::VCH> vload;
   kload.init(kh, kv_lim, wave, lane, kswz);
   vload.init(vh, kv_lim, wave, lane, vswz);
-  auto kslot = [&](int t) { return smem + (t % C::NKR) * C::K_BYTES; };
-  auto vslot = [&](int t) { return smem + C::NKR * C::K_BYTES + (t % C::NVR) * C::V_BYTES; };
+  // (tile indices are never negative: unsigned remainders, a mask for the power-of-two ring sizes)
+  auto kslot = [&](int t) { return smem + ((unsigned)t % C::NKR) * C::K_BYTES; };
+  auto vslot = [&](int t) { return smem + C::NKR * C::K_BYTES + ((unsigned)t % C::NVR) * C::V_BYTES; };
   // This wave's keys of tile t (rows kpart .. kpart + WBN - 1 of the slot). The K and V swizzles
   // repeat every 32 rows, so a part starting at row 32 reads like a tile of its own.
   auto kmine = [&](int t) { return kslot(t) + kpart * (DQK * 2); };
@@ -652,16 +653,19 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   // the defaults only V(j+1)); V(j-1), from the group of step j+1-NVR, came before it.
   // The barrier then publishes every wave's part and guarantees that all waves are done with step
   // j-1, whose slots (K(j), V(j-2)) the loads of step j overwrite.
-  u32x4 gk = {}, gv = {};
+  // The steps run in order j = 0, 1, ..., so the buffers of the tiles a step loads are the previous
+  // step's moved on by one tile (they start one tile before those of step 0).
+  int krem, vrem;
+  u32x4 gk = kload.rsrc_walk(kb0 + (C::KA - 1) * BN, krem), gv = vload.rsrc_walk(kb0 + (C::VA - 1) * BN, vrem);
   uint32_t gkl = 0, gvl = 0;
   auto sync_step = [&](int j) {
     wait_vmcnt<C::V_LOADS + (C::KA - 2) * (C::K_LOADS + C::V_LOADS)>();
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    gk = kload.rsrc(kb0 + (j + C::KA) * BN);
+    kload.advance(gk, krem);
     gkl = kload.lds(kslot(j + C::KA), wave);
-    gv = vload.rsrc(kb0 + (j + C::VA) * BN);
+    vload.advance(gv, vrem);
     gvl = vload.lds(vslot(j + C::VA), wave);
   };
   auto issue = [&](int k) {

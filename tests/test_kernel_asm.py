@@ -250,3 +250,16 @@ def test_no_scalar_memory_writes(asm_text, lbl_asm_text, decode_asm_text):
     # Every store and atomic goes through the vector memory path.
     for text in (asm_text, lbl_asm_text, decode_asm_text):
         assert not re.findall(r"\bs_(?:store|atomic|buffer_store|dcache_wb|dcache_discard)\w*", text)
+
+
+def test_buffer_descriptors_in_scalar_registers(asm_text, lbl_asm_text, decode_asm_text):
+    # A buffer instruction takes its resource descriptor from four SGPRs. The direct-to-LDS loads are
+    # inline assembly with a scalar-register constraint; should a descriptor value ever be computed in
+    # vector registers, the compiler substitutes the VGPRs into the instruction text instead of
+    # failing, and the load would address through an undefined descriptor.
+    for text in (asm_text, lbl_asm_text, decode_asm_text):
+        loads = re.findall(r"^\s*(buffer_\w+\s+[^\n]*)$", text, re.M)
+        assert loads
+        # operands: [vdata,] vaddr, srsrc, soffset: the descriptor is the operand before the last
+        bad = [ln for ln in loads if not re.search(r",\s*s\[\d+:\d+\],\s*[^,]+$", ln)]
+        assert not bad, bad[:5]
