@@ -155,7 +155,7 @@ struct Cfg {
   static constexpr int K_LOADS = BN * KCH / 64 / NWAVES;
   static constexpr int V_LOADS = BN * VCH / 64 / NWAVES;
   static_assert(DQK % 32 == 0 && DV % 64 == 0, "head dims: d_qk multiple of 32, d_v multiple of 64");
-  static_assert(BN == 64, "the step schedule assumes 64-key tiles (4 chunks of 16 keys)");
+  static_assert(BN % 64 == 0, "key tiles of whole 64-key units");
   static_assert((BN * KCH) % (64 * NWAVES) == 0 && (BN * VCH) % (64 * NWAVES) == 0, "tile split over waves");
   // KA - 1 <= VA <= KA: V(j-1) is issued before K(j+1) (so one counted wait covers both), and the
   // prologue's groups j = -KA .. -1 hold every tile's first load.
@@ -936,6 +936,18 @@ template <int DQK, int DV, bool CAUSAL>
 struct ShortInstance {
   using C = Cfg<DQK, DV, 64, 4, 1, CAUSAL, false, 2, DQK >= 128 ? 1 : 2, DQK >= 128 ? 2 : 6, 2, DQK >= 128 ? 3 : 4>;
 };
+// The short instance at d = 64 with 128-key tiles, for keys of at least kWideTileKeys: a step then
+// carries 32 MFMAs per wave instead of 16, over which the per-step waits, barrier, load issue and
+// addressing are spread (250 VGPRs; the 16 KiB tiles allow a V ring of 3 slots, 80 KiB per
+// workgroup). Measured against the 64-key tiles (one box, interleaved): 1.5-6 % faster from 1 536
+// keys on (BERT-Base and -Large S2048 1.05-1.06x, GPT-2 Small S8192 and S16384 1.02-1.03x), level at
+// 1 024, 1.5 % slower at 512 keys (workload 2), where the four steps of a block leave too little to
+// overlap with the pipeline's fill and drain.
+template <int DQK, int DV, bool CAUSAL>
+struct ShortWideInstance {
+  using C = Cfg<DQK, DV, 128, 4, 1, CAUSAL, false, 2, 2, 6, 2, 3>;
+};
+constexpr int kWideTileKeys = 1024;
 // Key halves: 4 waves as two sets of 2 x 32 query rows (64 row-heads per workgroup), each set taking
 // one 32-key half of every tile; three workgroups per CU at d = 64 (three waves per SIMD, 132 VGPRs,
 // 48 KiB of LDS each), two at d = 128 (208 VGPRs, 80 KiB). It runs problems whose grid of long-
@@ -1013,7 +1025,12 @@ hipError_t launch_instance(FwdParams p, Kind kind, hipStream_t stream) {
     if (kind == Kind::kHalf) return launch_cfg<typename HalfInstance<DQK, DV, CAUSAL>::C>(p, stream);
   }
   if constexpr (!SPLIT && DQK != 192) {
-    if (kind == Kind::kShort) return launch_cfg<typename ShortInstance<DQK, DV, CAUSAL>::C>(p, stream);
+    if (kind == Kind::kShort) {
+      if constexpr (DQK == 64) {
+        if (p.sk >= kWideTileKeys) return launch_cfg<typename ShortWideInstance<DQK, DV, CAUSAL>::C>(p, stream);
+      }
+      return launch_cfg<typename ShortInstance<DQK, DV, CAUSAL>::C>(p, stream);
+    }
   }
   return launch_cfg<typename Instance<DQK, DV, CAUSAL, SPLIT>::C>(p, stream);
 }

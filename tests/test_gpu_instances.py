@@ -16,7 +16,7 @@ import torch
 import paper_2609_21264_amd as fa
 import workloads as W
 from oracle import naive_attention
-from parity import check_full, compare, run_gpu, to_f64
+from parity import check_full, compare, rounding_bar, run_gpu, to_f64
 from test_gpu_parity import SMALL_CASES
 
 pytestmark = pytest.mark.gpu
@@ -141,3 +141,49 @@ def test_instance_boundary(d, causal, heads):
     assert rows(make(last + 1)) > rows(make(last))
     print(f"\n[case] {w} ({NAMES[rows(w)]})", flush=True)
     check_full(w)
+
+
+# At d = 64 the short instance takes 128-key tiles once Sk >= 1024 (the rows per workgroup stay 128):
+# cases in the short instance's range with such keys, every output element against the oracle.
+def _wide(name, Hq, Hkv, Sq, Sk, causal, seed, **kw):
+    return W.small(f"wide tiles {name}", dqk=64, dv=64, Hq=Hq, Hkv=Hkv, Sq=Sq, Sk=Sk, causal=causal, seed=seed, **kw)
+
+
+WIDE_TILES = [
+    _wide("ragged keys", 80, 80, 100, 1100, False, 301),
+    _wide("gqa4 whole tiles", 48, 12, 70, 1024, False, 302, B=2),
+    _wide("causal gqa4", 56, 14, 1300, 1300, True, 303),
+    _wide("causal Sq>Sk gqa2", 60, 30, 1500, 1100, True, 304),
+    _wide("causal Sq<Sk", 330, 330, 40, 2100, True, 305),
+    _wide("scale 0", 70, 70, 90, 1200, False, 306, scale=0.0),
+    _wide("negative scale gqa7", 70, 10, 90, 1500, False, 307, scale=-0.09),
+    _wide("sigma 2 causal gqa3", 330, 110, 128, 1280, True, 308, sigma=2.0),
+]
+
+
+@pytest.mark.parametrize("w", WIDE_TILES, ids=[w.name for w in WIDE_TILES])
+def test_short_instance_wide_tiles_match_oracle(w):
+    assert rows(w) == SHORT and w.Sk >= 1024
+    print(f"\n[case] {w}", flush=True)
+    q, k, v = W.make_inputs(w)
+    o, lse = run_gpu(q, k, v, w)
+    vf = to_f64(v)
+    o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), vf, w.scale, w.causal)
+    # sigma = 2: the bar derived from the bf16 rounding of P and O, as in the random sweep
+    compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name, max(1.0, w.sigma),
+            o_bar=rounding_bar(vf, w.Hq) if w.sigma > 1.0 else None)
+
+
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_short_instance_wide_tiles_rebase(causal):
+    """Rising maxima (keys scaled x4 .. x32 in four tiles of 128 keys) through the 128-key tiles."""
+    w = _wide("spikes", 330 if causal else 80, 110 if causal else 40, 64, 1500, causal, 309)
+    assert rows(w) == SHORT
+    q, k, v = W.make_inputs(w)
+    for key, factor in ((70, 4.0), (300, 8.0), (900, 16.0), (1490, 32.0)):
+        k[:, :, key] *= factor
+    print(f"\n[case] {w}", flush=True)
+    o, lse = run_gpu(q, k, v, w)
+    o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), to_f64(v), w.scale, causal)
+    assert np.nanmax(lse_ref) > 20.0
+    compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name)
