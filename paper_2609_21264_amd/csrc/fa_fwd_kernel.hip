@@ -861,12 +861,13 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
   }
 }
 
-// Entry kernels. The long instance reads everything from the argument block. The short instance,
-// whose workgroups are short chains on which the first loads' latency is felt, takes the values its
-// prologue needs first as leading scalar arguments, which the command processor preloads into SGPRs
-// before the first instruction (kernel-argument preloading, enabled at build time for the first 14
-// SGPRs of a kernel's leading scalar arguments), and issues its Q loads before it reads the argument
-// block. Preloading is kept off the long instance: it slows the launch of each wave, and on the 128K
+// Entry kernels. The long instance reads everything from the argument block. The instances with
+// several workgroups per CU (short and key halves), whose workgroups are short chains on which the
+// first loads' latency is felt, take the values their prologue needs first as leading scalar
+// arguments, which the command processor preloads into SGPRs before the first instruction
+// (kernel-argument preloading, enabled at build time for the first 14 SGPRs of a kernel's leading
+// scalar arguments), and issue their Q loads before they read the argument block. Preloading is kept
+// off the long instance: it slows the launch of each wave, and on the 128K
 // workload the spread-out starts of the workgroups that stream one K/V head through an XCD's L2
 // doubled the L2 misses, at no gain in time.
 template <class C>
