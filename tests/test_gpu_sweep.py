@@ -9,6 +9,8 @@ carry enough heads for the long kernel instance and a fifth enough for the short
 dimension and mask have one); the rest are small grids, which run the key-halves instance.
 """
 
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -78,9 +80,11 @@ def _check(w, **kw):
     torch.cuda.synchronize()
     vf = to_f64(v)
     o_ref, lse_ref = naive_attention(to_f64(q), to_f64(k), vf, w.scale, w.causal)
-    # unit-variance inputs (and narrower ones) meet the fixed bar; wider ones the bar derived from the
-    # bf16 rounding of P and O, which follows the output's magnitude
-    bar = rounding_bar(vf, w.Hq) if w.sigma > 1.0 else None
+    # unit-variance inputs (and narrower ones) at the default scale meet the fixed bar; wider inputs or
+    # a larger scale sharpen the softmax, so that O approaches single V rows: there the bar derived
+    # from the bf16 rounding of P and O, which follows the output's magnitude
+    sharp = w.sigma > 1.0 or abs(w.scale) > 1.0 / math.sqrt(w.dqk)
+    bar = rounding_bar(vf, w.Hq) if sharp else None
     compare(to_f64(o), lse.cpu().double().numpy(), o_ref, lse_ref, w.name, max(1.0, w.sigma), o_bar=bar)
 
 
