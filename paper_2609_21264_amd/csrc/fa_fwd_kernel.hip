@@ -674,18 +674,21 @@ __device__ __forceinline__ void fa_fwd_body(FwdParams p, const WorkMap wm) {
     else
       vload.issue_one(gv, gvl, k - C::K_LOADS);
   };
-  // Steps in pairs so that the two score tiles and the two P tiles swap roles without copies.
+  // Steps in pairs so that the two score tiles and the two P tiles swap roles without copies. A step
+  // masks its current tile from tile n_plain on; tile 0 was masked above when n_plain = 0, and masking
+  // it again in step 0 changes nothing (masked scores already hold mask_val), so the test needs no
+  // j > 0 term (one scalar compare per step instead of two compares and the mask logic).
   int j = 0;
   for (; j + 1 < nt; j += 2) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kmine(j + 1), j > 0 ? vmine(j - 1) : kmine(1), j > 0 && j >= n_plain,
+    st.step(sA, sB, pA, pB, kmine(j + 1), j > 0 ? vmine(j - 1) : kmine(1), j >= n_plain,
             kb0 + j * BN + kpart, issue);
     sync_step(j + 1);
     st.step(sB, sA, pB, pA, kmine(j + 2), vmine(j), j + 1 >= n_plain, kb0 + (j + 1) * BN + kpart, issue);
   }
   if (j < nt) {
     sync_step(j);
-    st.step(sA, sB, pA, pB, kmine(j + 1), j > 0 ? vmine(j - 1) : kmine(1), j > 0 && j >= n_plain,
+    st.step(sA, sB, pA, pB, kmine(j + 1), j > 0 ? vmine(j - 1) : kmine(1), j >= n_plain,
             kb0 + j * BN + kpart, issue);
   }
   if (nt > 0) {
