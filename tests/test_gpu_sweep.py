@@ -6,7 +6,9 @@ on; this file draws many more combinations of the same parameters at once (head 
 group size, batch, ragged query and key lengths, causal masking, scale and input spread) from a fixed
 seed, so that an interaction nobody thought of still meets the oracle. A quarter of the fused cases
 carry enough heads for the long kernel instance and a fifth enough for the short one (where the head
-dimension and mask have one); the rest are small grids, which run the key-halves instance.
+dimension and mask have one); the rest are small grids, which run the key-halves instance. A further
+set draws d = 64 problems in the short instance's range with 1024-3000 keys, where it takes 128-key
+tiles.
 """
 
 import math
@@ -69,6 +71,24 @@ def _cases(kind, n, seed):
 
 
 FUSED = _cases("fused", 160, 20260)
+
+
+def _draw_wide(rng, idx):
+    """d = 64 in the short instance's range with Sk >= 1024, where it takes 128-key tiles."""
+    g = GROUPS[rng.integers(len(GROUPS))]
+    causal = bool(rng.integers(2))
+    sq, sk = _length(rng, 1, 300), _length(rng, 1024, 3000)
+    per = g * -(-sq // 256)  # blocks per key/value head
+    hkv = -(-(HALF_MAX[(64, causal)] + 1) // per) + int(rng.integers(0, 3))
+    scale = None if rng.uniform() < 0.7 else float(rng.uniform(-0.3, 0.5))
+    sigma = float(rng.choice([1.0, 1.0, 0.5, 2.0]))
+    name = (f"wide{idx} B1 Hq{g * hkv} Hkv{hkv} Sq{sq} Sk{sk} d64{' causal' if causal else ''}"
+            f"{'' if scale is None else f' scale{scale:.3f}'} sigma{sigma:g}")
+    return W.small(name, B=1, Hq=g * hkv, Hkv=hkv, Sq=sq, Sk=sk, dqk=64, dv=64, causal=causal, scale=scale,
+                   seed=5400 + idx, sigma=sigma)
+
+
+WIDE = [_draw_wide(rng, i) for rng, i in ((np.random.default_rng(20263 + i), i) for i in range(24))]
 SPLIT = _cases("split", 48, 20261)
 DECODE = [w for w in _cases("decode", 96, 20262) if w.dqk != 192][:48]
 
@@ -106,6 +126,12 @@ def test_sweep_draws_every_instance_and_head_dimension():
 
 @pytest.mark.parametrize("w", FUSED, ids=[w.name for w in FUSED])
 def test_fused_sweep(w):
+    _check(w)
+
+
+@pytest.mark.parametrize("w", WIDE, ids=[w.name for w in WIDE])
+def test_wide_tile_sweep(w):
+    assert fa.fa_fwd_rows(w.B, w.Hq, w.Sq, w.dqk, w.dv, w.causal) == 128 and w.Sk >= 1024
     _check(w)
 
 
